@@ -1,0 +1,225 @@
+#!/usr/bin/env python3
+"""Throughput of the sparsity-preserved LoRA linear (forward + backward) on one GPU.
+
+One step = lors_forward + lors_backward_data + lors_backward_weight over one
+batch of seeded synthetic inputs already resident in HBM (every step of the
+layer runs in liblors.so; mask packing happens once, before timing).
+
+Prints ONE JSON line: whole-job TFLOP/s over the algorithmic flops
+6RCL + 8rRC per step, the fraction of the bf16 MFMA peak, peak bytes, the
+roofline entry of the dominant kernel (HIP-event durations on the launch
+stream) and the fp64 CPU oracle timed on the host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "masked-LoRA linear fwd+bwd TFLOP/s (bf16) and % of MFMA peak; peak bytes"
+DEFAULT_WORKLOAD = "llama2_7b_q_proj"
+# MI355X dense MFMA peaks in TFLOP/s: 256 CUs x 4 matrix cores x 2.4 GHz x
+# (1024 bf16 or 256 fp32 flops per clock per matrix core).  HBM3E 8 TB/s.
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum host time spent on the oracle sample")
+    return ap.parse_args()
+
+
+def to_dev(a, dtype, torch, np):
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def cpu_baseline(inp, args):
+    """The fp64 oracle on the same workload, timed on the host cores."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import bf16 as obf16
+    from oracle import lors as olors
+    from paper_2501_08582_amd import costs
+
+    wl = inp.wl
+    f = obf16.to_f64 if wl.dtype == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
+    # Bounded sample: the full weight with a slice of the tokens, sized so one
+    # oracle pass is a few seconds; repeated until --cpu-seconds have passed.
+    Ls = min(wl.L, 1024)
+    X, dY = f(inp.X[:Ls]), f(inp.dY[:Ls])
+    W, B, A = f(inp.W), f(inp.B), f(inp.A)
+    best, n, t_all = None, 0, time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        olors.forward(X, W, inp.M, B, A, wl.scale)
+        olors.backward(dY, X, W, inp.M, B, A, wl.scale)
+        dt = time.perf_counter() - t0
+        best = dt if best is None else min(best, dt)
+        n += 1
+        if time.perf_counter() - t_all >= args.cpu_seconds or n >= 20:
+            break
+    flops = costs.algorithmic_flops(wl.R, wl.C, Ls, wl.r)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+                  or [1])
+    return {
+        "value": flops / best / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"{wl.name}: full {wl.R}x{wl.C} weight, r={wl.r}, first {Ls} of {wl.L} tokens; "
+                   f"numpy fp64 forward+backward, best of {n} passes ({best:.2f} s each)"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer shards by tokens, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2501_08582_amd import _lib, costs, ops, synth
+
+    wl = synth.workload(args.workload)
+    inp = synth.make(wl)
+    dt = wl.dtype
+    R, C, L, r, s = wl.R, wl.C, wl.L, wl.r, wl.scale
+    fmt = ops.TWO_FOUR if wl.mask == "2:4" else ops.BITMAP
+    torch.cuda.set_device(0)
+
+    X, W, B, A, dY = (to_dev(t, dt, torch, np) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    Y = torch.empty((L, R), dtype=tdt, device="cuda")
+    dX = torch.empty((L, C), dtype=tdt, device="cuda")
+    dB = torch.empty((R, r), dtype=torch.float32, device="cuda")
+    dA = torch.empty((r, C), dtype=torch.float32, device="cuda")
+    p = _lib.problem(R, C, L, r, s, _lib.DTYPE_BF16 if dt == "bf16" else _lib.DTYPE_F32,
+                     _lib.MASK_2_4 if fmt == ops.TWO_FOUR else _lib.MASK_BITMAP)
+    ws = _lib.workspace_bytes(p)
+    assert ws == 0, "the library needs no workspace for these problems"
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    ptr = lambda t: t.data_ptr()  # noqa: E731
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        _lib.check(_lib.forward(p, ptr(X), ptr(W), ptr(M), ptr(B), ptr(A), None, ptr(Y), None, 0, sh),
+                   "lors_forward")
+        if ev is not None:
+            ev[1].record(stream)
+        _lib.check(_lib.backward_data(p, ptr(dY), ptr(W), ptr(M), ptr(B), ptr(A), ptr(dX), None, 0, sh),
+                   "lors_backward_data")
+        if ev is not None:
+            ev[2].record(stream)
+        _lib.check(_lib.backward_weight(p, ptr(dY), ptr(X), ptr(M), ptr(B), ptr(A), ptr(dB), ptr(dA),
+                                        None, None, 0, sh), "lors_backward_weight")
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Timed region: K steps bracketed by a device synchronisation on both
+    # sides; per-kernel events on the launch stream inside it.
+    torch.cuda.reset_peak_memory_stats()
+    mem0 = torch.cuda.memory_allocated()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    transient = torch.cuda.max_memory_allocated() - mem0
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+
+    per = {"fwd": [], "bwd_data": [], "bwd_weight": []}
+    for e in evs:
+        per["fwd"].append(e[0].elapsed_time(e[1]))
+        per["bwd_data"].append(e[1].elapsed_time(e[2]))
+        per["bwd_weight"].append(e[2].elapsed_time(e[3]))
+    avg = {k: sum(v) / len(v) for k, v in per.items()}
+    kflops = {"fwd": costs.fwd_flops(R, C, L, r), "bwd_data": costs.dx_flops(R, C, L, r),
+              "bwd_weight": costs.g_flops(R, C, L, r)}
+    kbytes = costs.min_hbm_bytes(R, C, L, r, elt=2 if dt == "bf16" else 4)
+    kbytes = {"fwd": kbytes["fwd"], "bwd_data": kbytes["dx"], "bwd_weight": kbytes["g"]}
+    kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel", "bwd_weight": "g_kernel (+ dA/dB clear)"}
+
+    flops = costs.algorithmic_flops(R, C, L, r)
+    value = flops / (ms_step * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[dt]
+    dom = max(avg, key=avg.get)
+    achieved = kflops[dom] / (avg[dom] * 1e-3) / 1e12
+    elt = 2 if dt == "bf16" else 4
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded, Llama-shaped; random-init weights and adapters)",
+        "config": {"workload": wl.name, "R": R, "C": C, "L": L, "r": r, "mask": wl.mask,
+                   "sparsity": wl.sparsity, "scale": s},
+        "pct_mfma_peak": round(100.0 * value / peak, 2),
+        "peak_bytes": {
+            "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),
+            "saved_activation": costs.saved_activation_bytes(C, L, elt),
+            "workspace": ws,
+            "transient_during_fwd_bwd": int(transient),
+            "merged_weight_would_be": elt * R * C,
+        },
+        "kernels": {k: {"ms": round(avg[k], 4), "tflops": round(kflops[k] / (avg[k] * 1e-3) / 1e12, 1),
+                        "pct_peak": round(100 * kflops[k] / (avg[k] * 1e-3) / 1e12 / peak, 2)}
+                    for k in avg},
+        "roofline": {
+            "kernel": kernel_names[dom],
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+            "algorithmic_bytes": kbytes[dom],
+        },
+        "wall_s_timed": round(wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(inp, args)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,224 @@
+/*
+ * lors.h -- C ABI of the sparsity-preserved LoRA linear for AMD MI355X (gfx950).
+ *
+ * The layer (LoRS, arXiv 2501.08582) fine-tunes a pruned weight W with a
+ * rank-r adapter while keeping W's sparsity pattern M:
+ *
+ *   forward   Y  = X . W'^T (+ bias),   W' = select(M, W + s.B.A, 0)
+ *   backward  dX = dY . W'                          (W' recomputed, never stored)
+ *             G  = select(M, dY^T . X, 0)           (never stored)
+ *             dB = s . G . A^T,   dA = s . B^T . G,  dbias = sum_tokens dY
+ *
+ * Sources: the SP-LoRA forward and backward step lists of Section 2.2 (Eq. 3),
+ * weight recompute of Section 2.3 (Algorithms 1 and 2), the scale factor and
+ * saved context of the Appendix A LoRS listing.  Readings taken where the
+ * paper is silent: s multiplies both adapter gradients (it is the exact
+ * derivative of the forward); the mask multiplies the whole sum W + s.B.A;
+ * masking is a select, so masked entries are +0; the mask stays on the weight
+ * gradient (exact gradient).  The paper's straight-through, re-associated
+ * backward (Section 2.3) is reserved under LORS_FLAG_BWD_STE.
+ *
+ * Names: B is R x r and A is r x C.  The paper calls the R x r adapter
+ * (calligraphic) A and the r x C adapter (calligraphic) B; this header uses
+ * the opposite, PEFT-style names.  The paper stores tokens as columns
+ * (X is C x L); here tokens are rows.
+ *
+ * Shapes and layouts -- every array is row-major and contiguous, and every
+ * pointer is 16-byte aligned:
+ *   X  L x C   W  R x C   B  R x r   A  r x C   bias R
+ *   Y, dY  L x R          dX  L x C
+ *   dB  R x r (float32)   dA  r x C (float32)    dbias  R (float32)
+ *   packed mask  R x ceil(C/32) uint32 words (layouts below)
+ * The problem dtype (bf16 or fp32) applies to X, W, B, A, bias, Y, dY, dX.
+ * L (tokens) is the product of all leading dimensions of the activation.
+ *
+ * Arithmetic (bf16): W + s.B.A is formed in fp32 from the bf16 operands and
+ * rounded once to bf16 (nearest-even) before the main product; all products
+ * accumulate in fp32; Y and dX are rounded to bf16 (nearest-even); G is
+ * rounded to bf16 before the two rank-r products; dA, dB, dbias stay fp32.
+ * The fp32 dtype keeps every intermediate in fp32 (a debug/reference path).
+ *
+ * Ownership: the caller owns every buffer.  The library never allocates
+ * device memory; its scratch needs are reported by lors_workspace_bytes.
+ * Pointers must stay valid until the work queued on `stream` completes; the
+ * library keeps nothing after a call returns.  Inputs are read only.  Outputs
+ * are overwritten, never accumulated into, and must not overlap any input or
+ * each other (LORS_ERR_ALIAS).  `stream` is a hipStream_t (NULL = default).
+ *
+ * Errors: every entry point returns a lors_status_t; nothing prints, throws or
+ * aborts.  Arguments are validated on the host in the order
+ *   null -> dtype/format -> shape/range -> alignment -> alias -> workspace
+ * before any HIP call, so a rejected call has no side effect.  With L == 0
+ * the token-sized arrays (X, Y, dY, dX) may be NULL.  Kernel-launch
+ * failures return LORS_ERR_HIP.  Compute calls are asynchronous on `stream`.
+ */
+#ifndef LORS_H
+#define LORS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lors_status {
+    LORS_OK = 0,
+    LORS_ERR_NULL = 1,          /* a required pointer is NULL */
+    LORS_ERR_DTYPE = 2,         /* unknown dtype */
+    LORS_ERR_SHAPE = 3,         /* negative/zero extent where not allowed, r out of range */
+    LORS_ERR_MASK_FORMAT = 4,   /* unknown mask format, or 2:4 with C % 4 != 0 */
+    LORS_ERR_ALIGN = 5,         /* a pointer is not 16-byte aligned */
+    LORS_ERR_ALIAS = 6,         /* an output overlaps an input or another output */
+    LORS_ERR_WORKSPACE = 7,     /* workspace smaller than lors_workspace_bytes */
+    LORS_ERR_UNSUPPORTED = 8,   /* valid but unsupported: see lors_problem_t */
+    LORS_ERR_NOT_2_4 = 9,       /* host packer: a group does not keep exactly 2 of 4 */
+    LORS_ERR_HIP = 10           /* a HIP runtime call or kernel launch failed */
+} lors_status_t;
+
+typedef enum lors_dtype {
+    LORS_DTYPE_BF16 = 0,
+    LORS_DTYPE_F32 = 1
+} lors_dtype_t;
+
+/*
+ * Packed mask layouts (the paper keeps M as a dense boolean, `weight != 0`;
+ * the packing is this library's own).  Both use ceil(C/32) uint32 words per
+ * row, i.e. C/8 bytes per row when C % 32 == 0.
+ *   LORS_MASK_BITMAP: element (i, j) is bit j % 32 (least significant first)
+ *     of word i*ceil(C/32) + j/32.  Padding bits past C must be 0.
+ *   LORS_MASK_2_4: needs C % 4 == 0.  Group g of row i (columns 4g..4g+3)
+ *     keeps exactly two positions p0 < p1 and stores the nibble p0 | p1 << 2
+ *     at bits 4*(g % 8) of word i*ceil(C/32) + g/8.  Unused nibbles are 0.
+ */
+typedef enum lors_mask_format {
+    LORS_MASK_BITMAP = 0,
+    LORS_MASK_2_4 = 1
+} lors_mask_format_t;
+
+/* Reserved: the straight-through, re-associated backward of Section 2.3
+ * (Algorithm 2).  Currently rejected with LORS_ERR_UNSUPPORTED. */
+#define LORS_FLAG_BWD_STE 0x1u
+
+/*
+ * Problem description.
+ *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
+ *   1 <= r <= 128, every extent < 2^31, scale finite.
+ *   bf16: R % 8 == 0 and C % 8 == 0;  fp32: R % 4 == 0 and C % 4 == 0
+ *   (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
+ */
+typedef struct lors_problem {
+    int64_t R;
+    int64_t C;
+    int64_t L;
+    int64_t r;
+    float scale;
+    int32_t dtype;        /* lors_dtype_t */
+    int32_t mask_format;  /* lors_mask_format_t */
+    uint32_t flags;       /* must be 0 */
+} lors_problem_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* lors_status_string(int status);
+
+/* ABI version: major * 10000 + minor * 100 + patch. */
+int lors_version(void);
+
+/* Bytes of a packed R x C mask (either layout): 4 * R * ceil(C/32). */
+size_t lors_mask_packed_bytes(int64_t R, int64_t C);
+
+/*
+ * Device mask packing.  `dense` is an R x C uint8 device array (nonzero =
+ * kept); `packed` receives lors_mask_packed_bytes(R, C) bytes.  For
+ * LORS_MASK_2_4, `first_bad` (device, one int64) is required and receives the
+ * linear index i*(C/4)+g of the first group that does not keep exactly two
+ * entries, or -1 if every group is valid; for the bitmap it may be NULL (it is
+ * then left untouched) or receives -1.  Asynchronous on `stream`.
+ * The mask M is the one of Section 2.1 and Algorithm 1 (kept = nonzero).
+ */
+lors_status_t lors_mask_pack(const uint8_t* dense, int64_t R, int64_t C,
+                             int32_t mask_format, uint32_t* packed,
+                             int64_t* first_bad, void* stream);
+
+/* Device unpacking: packed -> dense uint8 0/1 (R x C).  Asynchronous. */
+lors_status_t lors_mask_unpack(const uint32_t* packed, int64_t R, int64_t C,
+                               int32_t mask_format, uint8_t* dense, void* stream);
+
+/*
+ * Device mask derivation M = (W != 0) from the weight itself, as the paper's
+ * algorithms and listing do (`weight != 0`); -0 counts as zero.  W has dtype
+ * `dtype`.  `first_bad` as for lors_mask_pack.  Asynchronous.
+ */
+lors_status_t lors_mask_from_weight(const void* W, int32_t dtype, int64_t R,
+                                    int64_t C, int32_t mask_format,
+                                    uint32_t* packed, int64_t* first_bad,
+                                    void* stream);
+
+/* Host twins of lors_mask_pack / lors_mask_unpack on host memory.  The
+ * packer returns LORS_ERR_NOT_2_4 (and *first_bad, if non-NULL, the group
+ * index) for an invalid 2:4 mask; `packed` is then unspecified. */
+lors_status_t lors_mask_pack_host(const uint8_t* dense, int64_t R, int64_t C,
+                                  int32_t mask_format, uint32_t* packed,
+                                  int64_t* first_bad);
+lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C,
+                                    int32_t mask_format, uint8_t* dense);
+
+/* Device scratch bytes lors_forward/lors_backward need for problem p
+ * (currently 0 for every supported problem; (size_t)-1 if p is invalid). */
+size_t lors_workspace_bytes(const lors_problem_t* p);
+
+/*
+ * Forward: Y = X . W'^T (+ bias), W' = select(M, W + s.B.A, 0)
+ * (Eq. 3 and Algorithm 1; W' exists only tile by tile in on-chip memory).
+ * `bias` may be NULL.  Inputs X, W, M_packed, B, A are what a training
+ * framework keeps for the backward (the listing saves x and the parameters;
+ * W' and a dense mask are not kept).
+ */
+lors_status_t lors_forward(const lors_problem_t* p, const void* X,
+                           const void* W, const uint32_t* M_packed,
+                           const void* B, const void* A, const void* bias,
+                           void* Y, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * Backward (SP-LoRA backward list of Section 2.2 with the weight recompute of
+ * Algorithm 2): dX = dY . W' (skipped if dX is NULL), G = select(M, dY^T.X, 0),
+ * dB = s.G.A^T, dA = s.B^T.G, dbias = column sums of dY (skipped if NULL).
+ * dB, dA, dbias are fp32 and are overwritten.  Their summation order across
+ * tiles is not fixed (fp32 atomics), so they can differ run to run in the
+ * last bits; dX is bitwise reproducible.
+ */
+lors_status_t lors_backward(const lors_problem_t* p, const void* dY,
+                            const void* X, const void* W,
+                            const uint32_t* M_packed, const void* B,
+                            const void* A, void* dX, float* dB, float* dA,
+                            float* dbias, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * The two halves of lors_backward as separate calls, for callers that need
+ * only one of them (a frozen first layer needs no dX; frozen adapters need no
+ * dB/dA) or that schedule them on different streams.  Arguments, layouts and
+ * errors as for lors_backward; dX is required by lors_backward_data, dB and
+ * dA by lors_backward_weight.
+ *   lors_backward_data:   dX = dY . W'  (W' recomputed tile by tile;
+ *                         the dX step of Section 2.2, Algorithm 2)
+ *   lors_backward_weight: G = select(M, dY^T.X, 0) (I_w^4, I_w^5 of Section
+ *                         2.2), dB = s.G.A^T, dA = s.B^T.G, dbias
+ */
+lors_status_t lors_backward_data(const lors_problem_t* p, const void* dY,
+                                 const void* W, const uint32_t* M_packed,
+                                 const void* B, const void* A, void* dX,
+                                 void* workspace, size_t workspace_bytes,
+                                 void* stream);
+lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY,
+                                   const void* X, const uint32_t* M_packed,
+                                   const void* B, const void* A, float* dB,
+                                   float* dA, float* dbias, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LORS_H */

@@ -1,0 +1,358 @@
+// C ABI of the sparsity-preserved LoRA linear: argument validation, dispatch
+// to the gfx950 kernels, and the host twins of the mask packer.
+//
+// Validation runs entirely on the host, in a fixed order (null, dtype/format,
+// shape/range, alignment, alias, workspace), before any HIP call, so every
+// rejected call is free of side effects.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "lors.h"
+#include "kernels.hpp"
+
+namespace {
+
+constexpr int64_t kMaxExtent = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxRank = 128;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void* p, int64_t bytes) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Range{lo, lo + static_cast<uintptr_t>(bytes > 0 ? bytes : 0)};
+}
+
+bool overlap(Range a, Range b) {
+    if (a.lo == a.hi || b.lo == b.hi) return false;  // empty ranges never overlap
+    return a.lo < b.hi && b.lo < a.hi;
+}
+
+int64_t words_per_row(int64_t C) { return (C + 31) / 32; }
+
+int64_t elt_size(int32_t dtype) { return dtype == LORS_DTYPE_BF16 ? 2 : 4; }
+
+bool valid_dtype(int32_t d) { return d == LORS_DTYPE_BF16 || d == LORS_DTYPE_F32; }
+bool valid_format(int32_t f) { return f == LORS_MASK_BITMAP || f == LORS_MASK_2_4; }
+
+// Problem-level checks shared by forward/backward/workspace query, in the
+// documented order (dtype/format, then shape/range).
+lors_status_t check_problem(const lors_problem_t* p) {
+    if (!valid_dtype(p->dtype)) return LORS_ERR_DTYPE;
+    if (!valid_format(p->mask_format)) return LORS_ERR_MASK_FORMAT;
+    if (p->R < 1 || p->C < 1 || p->L < 0 || p->r < 1 || p->r > kMaxRank) return LORS_ERR_SHAPE;
+    if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
+    if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
+    if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
+    if (p->flags != 0u) return LORS_ERR_UNSUPPORTED;
+    const int64_t row_align = p->dtype == LORS_DTYPE_BF16 ? 8 : 4;
+    if (p->R % row_align != 0 || p->C % row_align != 0) return LORS_ERR_UNSUPPORTED;
+    if (p->dtype == LORS_DTYPE_F32) {
+        // The fp32 kernels put token tiles of 64 on the second grid axis.
+        if ((p->L + 63) / 64 > 65535 || (p->R + 63) / 64 > 65535) return LORS_ERR_UNSUPPORTED;
+    }
+    // Tile counts of the bf16 kernels must fit a 32-bit grid.
+    const int64_t t256 = ((p->L + 255) / 256) * ((p->R + 255) / 256);
+    const int64_t t256x = ((p->L + 255) / 256) * ((p->C + 255) / 256);
+    const int64_t t256g = ((p->R + 255) / 256) * ((p->C + 255) / 256);
+    if (t256 > kMaxExtent || t256x > kMaxExtent || t256g > kMaxExtent) return LORS_ERR_UNSUPPORTED;
+    return LORS_OK;
+}
+
+lors_status_t from_hip(hipError_t e) { return e == hipSuccess ? LORS_OK : LORS_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* lors_status_string(int status) {
+    switch (status) {
+        case LORS_OK: return "LORS_OK";
+        case LORS_ERR_NULL: return "LORS_ERR_NULL: a required pointer is NULL";
+        case LORS_ERR_DTYPE: return "LORS_ERR_DTYPE: unknown dtype";
+        case LORS_ERR_SHAPE: return "LORS_ERR_SHAPE: extent or rank out of range";
+        case LORS_ERR_MASK_FORMAT: return "LORS_ERR_MASK_FORMAT: unknown mask format or 2:4 with C % 4 != 0";
+        case LORS_ERR_ALIGN: return "LORS_ERR_ALIGN: pointer not 16-byte aligned";
+        case LORS_ERR_ALIAS: return "LORS_ERR_ALIAS: an output overlaps an input or another output";
+        case LORS_ERR_WORKSPACE: return "LORS_ERR_WORKSPACE: workspace too small";
+        case LORS_ERR_UNSUPPORTED: return "LORS_ERR_UNSUPPORTED: valid but unsupported problem";
+        case LORS_ERR_NOT_2_4: return "LORS_ERR_NOT_2_4: a group does not keep exactly 2 of 4";
+        case LORS_ERR_HIP: return "LORS_ERR_HIP: HIP runtime or kernel launch failure";
+        default: return "LORS: unknown status";
+    }
+}
+
+int lors_version(void) { return 10000; }
+
+size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
+    if (R < 0 || C < 0) return 0;
+    return static_cast<size_t>(R * words_per_row(C) * 4);
+}
+
+size_t lors_workspace_bytes(const lors_problem_t* p) {
+    if (p == nullptr || check_problem(p) != LORS_OK) return static_cast<size_t>(-1);
+    return 0;
+}
+
+// ---------------------------------------------------------------------------
+// masks
+// ---------------------------------------------------------------------------
+
+static lors_status_t check_mask_args(int64_t R, int64_t C, int32_t fmt) {
+    if (!valid_format(fmt)) return LORS_ERR_MASK_FORMAT;
+    if (R < 0 || C < 0 || R > kMaxExtent || C > kMaxExtent) return LORS_ERR_SHAPE;
+    if (fmt == LORS_MASK_2_4 && (C % 4) != 0) return LORS_ERR_MASK_FORMAT;
+    return LORS_OK;
+}
+
+lors_status_t lors_mask_pack(const uint8_t* dense, int64_t R, int64_t C, int32_t mask_format,
+                             uint32_t* packed, int64_t* first_bad, void* stream) {
+    if (dense == nullptr || packed == nullptr) return LORS_ERR_NULL;
+    if (mask_format == LORS_MASK_2_4 && first_bad == nullptr) return LORS_ERR_NULL;
+    lors_status_t st = check_mask_args(R, C, mask_format);
+    if (st != LORS_OK) return st;
+    if (!aligned16(dense) || !aligned16(packed) || (first_bad && (reinterpret_cast<uintptr_t>(first_bad) & 7u)))
+        return LORS_ERR_ALIGN;
+    const Range out = range_of(packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C)));
+    if (overlap(out, range_of(dense, R * C)) ||
+        (first_bad && (overlap(range_of(first_bad, 8), out) || overlap(range_of(first_bad, 8), range_of(dense, R * C)))))
+        return LORS_ERR_ALIAS;
+    return from_hip(lors::launch_mask_pack(dense, R, C, mask_format == LORS_MASK_2_4, packed, first_bad,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+lors_status_t lors_mask_unpack(const uint32_t* packed, int64_t R, int64_t C, int32_t mask_format,
+                               uint8_t* dense, void* stream) {
+    if (dense == nullptr || packed == nullptr) return LORS_ERR_NULL;
+    lors_status_t st = check_mask_args(R, C, mask_format);
+    if (st != LORS_OK) return st;
+    if (!aligned16(dense) || !aligned16(packed)) return LORS_ERR_ALIGN;
+    if (overlap(range_of(dense, R * C), range_of(packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C)))))
+        return LORS_ERR_ALIAS;
+    return from_hip(lors::launch_mask_unpack(packed, R, C, mask_format == LORS_MASK_2_4, dense,
+                                             static_cast<hipStream_t>(stream)));
+}
+
+lors_status_t lors_mask_from_weight(const void* W, int32_t dtype, int64_t R, int64_t C, int32_t mask_format,
+                                    uint32_t* packed, int64_t* first_bad, void* stream) {
+    if (W == nullptr || packed == nullptr) return LORS_ERR_NULL;
+    if (mask_format == LORS_MASK_2_4 && first_bad == nullptr) return LORS_ERR_NULL;
+    if (!valid_dtype(dtype)) return LORS_ERR_DTYPE;
+    lors_status_t st = check_mask_args(R, C, mask_format);
+    if (st != LORS_OK) return st;
+    if (!aligned16(W) || !aligned16(packed) || (first_bad && (reinterpret_cast<uintptr_t>(first_bad) & 7u)))
+        return LORS_ERR_ALIGN;
+    const Range out = range_of(packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C)));
+    const Range w = range_of(W, R * C * elt_size(dtype));
+    if (overlap(out, w) || (first_bad && (overlap(range_of(first_bad, 8), out) || overlap(range_of(first_bad, 8), w))))
+        return LORS_ERR_ALIAS;
+    return from_hip(lors::launch_mask_from_weight(W, dtype == LORS_DTYPE_BF16, R, C, mask_format == LORS_MASK_2_4,
+                                                  packed, first_bad, static_cast<hipStream_t>(stream)));
+}
+
+lors_status_t lors_mask_pack_host(const uint8_t* dense, int64_t R, int64_t C, int32_t mask_format,
+                                  uint32_t* packed, int64_t* first_bad) {
+    if ((dense == nullptr && R * C > 0) || (packed == nullptr && R * C > 0)) return LORS_ERR_NULL;
+    lors_status_t st = check_mask_args(R, C, mask_format);
+    if (st != LORS_OK) return st;
+    const int64_t wpr = words_per_row(C);
+    if (first_bad) *first_bad = -1;
+    for (int64_t i = 0; i < R; ++i) {
+        const uint8_t* row = dense + i * C;
+        for (int64_t w = 0; w < wpr; ++w) {
+            uint32_t word = 0;
+            if (mask_format == LORS_MASK_BITMAP) {
+                for (int64_t e = 0; e < 32 && 32 * w + e < C; ++e)
+                    if (row[32 * w + e]) word |= 1u << e;
+            } else {
+                for (int64_t n = 0; n < 8; ++n) {
+                    const int64_t g = 8 * w + n;
+                    if (g >= C / 4) break;
+                    int kept[4] = {0, 0, 0, 0};
+                    int nk = 0;
+                    for (int q = 0; q < 4; ++q)
+                        if (row[4 * g + q]) kept[nk++] = q;
+                    if (nk != 2) {
+                        if (first_bad) *first_bad = i * (C / 4) + g;
+                        return LORS_ERR_NOT_2_4;
+                    }
+                    word |= static_cast<uint32_t>(kept[0] | (kept[1] << 2)) << (4 * n);
+                }
+            }
+            packed[i * wpr + w] = word;
+        }
+    }
+    return LORS_OK;
+}
+
+lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C, int32_t mask_format,
+                                    uint8_t* dense) {
+    if ((dense == nullptr && R * C > 0) || (packed == nullptr && R * C > 0)) return LORS_ERR_NULL;
+    lors_status_t st = check_mask_args(R, C, mask_format);
+    if (st != LORS_OK) return st;
+    const int64_t wpr = words_per_row(C);
+    for (int64_t i = 0; i < R; ++i) {
+        for (int64_t j = 0; j < C; ++j) {
+            const uint32_t word = packed[i * wpr + j / 32];
+            uint8_t v;
+            if (mask_format == LORS_MASK_BITMAP) {
+                v = static_cast<uint8_t>((word >> (j % 32)) & 1u);
+            } else {
+                const uint32_t nib = (word >> (4 * ((j / 4) % 8))) & 0xFu;
+                const uint32_t q = static_cast<uint32_t>(j % 4);
+                v = static_cast<uint8_t>((nib & 3u) == q || (nib >> 2) == q);
+            }
+            dense[i * C + j] = v;
+        }
+    }
+    return LORS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// forward / backward
+// ---------------------------------------------------------------------------
+
+lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W, const uint32_t* M_packed,
+                           const void* B, const void* A, const void* bias, void* Y, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    if (p == nullptr) return LORS_ERR_NULL;
+    const bool tok = p->L != 0;  // with no tokens the activations may be NULL
+    if ((tok && (X == nullptr || Y == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
+        A == nullptr)
+        return LORS_ERR_NULL;
+    lors_status_t st = check_problem(p);
+    if (st != LORS_OK) return st;
+    if (!aligned16(X) || !aligned16(W) || !aligned16(M_packed) || !aligned16(B) || !aligned16(A) ||
+        !aligned16(Y) || (bias && !aligned16(bias)))
+        return LORS_ERR_ALIGN;
+    const int64_t es = elt_size(p->dtype);
+    const int64_t R = p->R, C = p->C, L = p->L, r = p->r;
+    const Range y = range_of(Y, L * R * es);
+    const Range ins[] = {range_of(X, L * C * es), range_of(W, R * C * es),
+                         range_of(M_packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C))),
+                         range_of(B, R * r * es), range_of(A, r * C * es),
+                         bias ? range_of(bias, R * es) : Range{0, 0}};
+    for (const Range& in : ins)
+        if (overlap(y, in)) return LORS_ERR_ALIAS;
+    if (workspace_bytes < lors_workspace_bytes(p)) return LORS_ERR_WORKSPACE;
+    (void)workspace;
+
+    lors::LayerArgs a{};
+    a.R = R; a.C = C; a.L = L; a.r = r;
+    a.scale = p->scale;
+    a.two_four = p->mask_format == LORS_MASK_2_4;
+    a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.bias = bias; a.Y = Y;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_fwd_bf16(a, s) : lors::launch_fwd_f32(a, s));
+}
+
+namespace {
+
+// Shared validation of the three backward entry points.  Null pointers of
+// optional outputs have been mapped to nullptr by the caller.
+lors_status_t check_backward(const lors_problem_t* p, const void* dY, const void* X, const void* W,
+                             const uint32_t* M_packed, const void* B, const void* A, void* dX, float* dB,
+                             float* dA, float* dbias, size_t workspace_bytes) {
+    lors_status_t st = check_problem(p);
+    if (st != LORS_OK) return st;
+    const void* all[] = {dY, X, W, M_packed, B, A, dX, dB, dA, dbias};
+    for (const void* q : all)
+        if (q && !aligned16(q)) return LORS_ERR_ALIGN;
+    const int64_t es = elt_size(p->dtype);
+    const int64_t R = p->R, C = p->C, L = p->L, r = p->r;
+    const Range ins[] = {range_of(dY, L * R * es), X ? range_of(X, L * C * es) : Range{0, 0},
+                         W ? range_of(W, R * C * es) : Range{0, 0},
+                         range_of(M_packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C))),
+                         range_of(B, R * r * es), range_of(A, r * C * es)};
+    const Range outs[] = {dX ? range_of(dX, L * C * es) : Range{0, 0}, dB ? range_of(dB, R * r * 4) : Range{0, 0},
+                          dA ? range_of(dA, r * C * 4) : Range{0, 0}, dbias ? range_of(dbias, R * 4) : Range{0, 0}};
+    for (int o = 0; o < 4; ++o) {
+        for (const Range& in : ins)
+            if (overlap(outs[o], in)) return LORS_ERR_ALIAS;
+        for (int o2 = o + 1; o2 < 4; ++o2)
+            if (overlap(outs[o], outs[o2])) return LORS_ERR_ALIAS;
+    }
+    if (workspace_bytes < lors_workspace_bytes(p)) return LORS_ERR_WORKSPACE;
+    return LORS_OK;
+}
+
+lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* X, const void* W,
+                           const uint32_t* M_packed, const void* B, const void* A, void* dX, float* dB,
+                           float* dA, float* dbias) {
+    lors::LayerArgs a{};
+    a.R = p->R; a.C = p->C; a.L = p->L; a.r = p->r;
+    a.scale = p->scale;
+    a.two_four = p->mask_format == LORS_MASK_2_4;
+    a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.dY = dY;
+    a.dX = dX; a.dB = dB; a.dA = dA; a.dbias = dbias;
+    return a;
+}
+
+hipError_t run_weight(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
+    hipError_t e = lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
+    if (e == hipSuccess) e = bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
+    if (e == hipSuccess) e = bf16 ? lors::launch_dbias_bf16(a, s) : lors::launch_dbias_f32(a, s);
+    return e;
+}
+
+}  // namespace
+
+lors_status_t lors_backward(const lors_problem_t* p, const void* dY, const void* X, const void* W,
+                            const uint32_t* M_packed, const void* B, const void* A, void* dX, float* dB,
+                            float* dA, float* dbias, void* workspace, size_t workspace_bytes, void* stream) {
+    if (p == nullptr) return LORS_ERR_NULL;
+    const bool tok = p->L != 0;
+    if ((tok && (dY == nullptr || X == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
+        A == nullptr || dB == nullptr || dA == nullptr)
+        return LORS_ERR_NULL;
+    lors_status_t st = check_backward(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace_bytes);
+    if (st != LORS_OK) return st;
+    (void)workspace;
+    const lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool bf16 = p->dtype == LORS_DTYPE_BF16;
+    hipError_t e = hipSuccess;
+    if (dX) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
+    if (e == hipSuccess) e = run_weight(a, bf16, s);
+    return from_hip(e);
+}
+
+lors_status_t lors_backward_data(const lors_problem_t* p, const void* dY, const void* W, const uint32_t* M_packed,
+                                 const void* B, const void* A, void* dX, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+    if (p == nullptr) return LORS_ERR_NULL;
+    const bool tok = p->L != 0;
+    if ((tok && (dY == nullptr || dX == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
+        A == nullptr)
+        return LORS_ERR_NULL;
+    lors_status_t st = check_backward(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr,
+                                      workspace_bytes);
+    if (st != LORS_OK) return st;
+    (void)workspace;
+    const lors::LayerArgs a = layer_args(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s));
+}
+
+lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY, const void* X, const uint32_t* M_packed,
+                                   const void* B, const void* A, float* dB, float* dA, float* dbias, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    if (p == nullptr) return LORS_ERR_NULL;
+    const bool tok = p->L != 0;
+    if ((tok && (dY == nullptr || X == nullptr)) || M_packed == nullptr || B == nullptr || A == nullptr ||
+        dB == nullptr || dA == nullptr)
+        return LORS_ERR_NULL;
+    lors_status_t st = check_backward(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias, workspace_bytes);
+    if (st != LORS_OK) return st;
+    (void)workspace;
+    const lors::LayerArgs a = layer_args(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias);
+    return from_hip(run_weight(a, p->dtype == LORS_DTYPE_BF16, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// Device-side building blocks shared by the gfx950 kernels: vector types,
+// the bf16 MFMA wrapper, bf16 conversions and the packed-mask decoders.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lors {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16).
+// Operand layout per lane l (h = l / 32):
+//   A: row l % 32, k = 8h .. 8h+7     B: column l % 32, k = 8h .. 8h+7
+//   D: element v (0..15) is row 8*(v/4) + 4h + (v%4), column l % 32.
+__device__ __forceinline__ f32x16 mfma_32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h16) {
+    return __uint_as_float(h16 << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 (gfx950 converts in hardware).
+__device__ __forceinline__ __bf16 to_bf16(float f) { return (__bf16)f; }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    bf16x2 v;
+    v[0] = (__bf16)lo;
+    v[1] = (__bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ uint16_t bf16_bits(float f) {
+    return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+// Keep-bits of 4 consecutive columns starting at bit position `pos` (a
+// multiple of 4, 0..28) of a packed mask word.  Bit q of the result says
+// whether column pos+q is kept.
+//   bitmap: the four bits themselves.
+//   2:4:    the group's nibble p0 | p1 << 2 names the two kept positions.
+template <bool kTwoFour>
+__device__ __forceinline__ uint32_t keep4(uint32_t word, uint32_t pos) {
+    uint32_t nib = (word >> pos) & 0xFu;
+    if constexpr (kTwoFour) {
+        return (1u << (nib & 3u)) | (1u << (nib >> 2));
+    } else {
+        return nib;
+    }
+}
+
+// Keep-bit of column `col` (0..31 within the word).
+template <bool kTwoFour>
+__device__ __forceinline__ uint32_t keep1(uint32_t word, uint32_t col) {
+    uint32_t q = col & 3u;
+    return (keep4<kTwoFour>(word, col & ~3u) >> q) & 1u;
+}
+
+__device__ __forceinline__ uint32_t ceil_div_u32(uint32_t a, uint32_t b) {
+    return (a + b - 1) / b;
+}
+
+// Map a workgroup id to an output tile (tm, tn).
+// MI355X dispatches consecutive workgroup ids round-robin over its 8 XCDs,
+// each with a private L2.  When the grid divides evenly, ids are first
+// regrouped so that every XCD receives one contiguous range of logical tiles;
+// the logical order then walks `group_m` tile rows at a time, so the tiles an
+// XCD holds at once share few operand panels.
+__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int group_m,
+                                            int& tm, int& tn) {
+    const int total = tiles_m * tiles_n;
+    int t = bid;
+    if ((total & 7) == 0) t = (bid & 7) * (total >> 3) + (bid >> 3);
+    const int per_group = group_m * tiles_n;
+    const int g = t / per_group;
+    const int first_m = g * group_m;
+    const int gsz = min(tiles_m - first_m, group_m);
+    const int within = t - g * per_group;
+    tm = first_m + within % gsz;
+    tn = within / gsz;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// 16-bit element e (0..7) of a 16-byte vector.
+__device__ __forceinline__ uint32_t u16_at(u32x4 v, int e) {
+    return (v[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;
+}
+
+}  // namespace lors

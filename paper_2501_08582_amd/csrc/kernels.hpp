@@ -1,0 +1,52 @@
+// Internal launcher interface between the C ABI (abi.cpp) and the kernels.
+// Every launcher assumes its arguments were validated by the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lors {
+
+struct LayerArgs {
+    int64_t R, C, L, r;
+    float scale;
+    bool two_four;          // packed mask layout: 2:4 codes (else bitmap)
+    const void* X;          // L x C
+    const void* W;          // R x C
+    const uint32_t* M;      // R x ceil(C/32)
+    const void* B;          // R x r
+    const void* A;          // r x C
+    const void* bias;       // R or nullptr
+    const void* dY;         // L x R
+    void* Y;                // L x R
+    void* dX;               // L x C or nullptr
+    float* dB;              // R x r
+    float* dA;              // r x C
+    float* dbias;           // R or nullptr
+};
+
+// bf16 path
+hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_dbias_bf16(const LayerArgs& a, hipStream_t s);
+
+// fp32 path
+hipError_t launch_fwd_f32(const LayerArgs& a, hipStream_t s);
+hipError_t launch_dx_f32(const LayerArgs& a, hipStream_t s);
+hipError_t launch_g_f32(const LayerArgs& a, hipStream_t s);
+hipError_t launch_dbias_f32(const LayerArgs& a, hipStream_t s);
+
+// helpers
+hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t s);
+// clears two fp32 buffers with one launch
+hipError_t launch_zero2_f32(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);
+hipError_t launch_mask_pack(const uint8_t* dense, int64_t R, int64_t C, bool two_four,
+                            uint32_t* packed, int64_t* first_bad, hipStream_t s);
+hipError_t launch_mask_from_weight(const void* W, bool w_is_bf16, int64_t R, int64_t C,
+                                   bool two_four, uint32_t* packed, int64_t* first_bad,
+                                   hipStream_t s);
+hipError_t launch_mask_unpack(const uint32_t* packed, int64_t R, int64_t C, bool two_four,
+                              uint8_t* dense, hipStream_t s);
+
+}  // namespace lors

@@ -1,0 +1,238 @@
+// Mask packing (dense 0/1 or weight != 0 -> 1 bit per element), unpacking,
+// output clearing and the bias gradient.
+//
+// Packed layouts (the paper keeps the mask as a dense boolean; the packing is
+// this library's own):
+//   bitmap: element (i, j) is bit j % 32 of word i*ceil(C/32) + j/32
+//   2:4:    group g of row i keeps p0 < p1; nibble p0 | p1 << 2 at bits
+//           4*(g % 8) of word i*ceil(C/32) + g/8
+// One thread produces one packed word from 32 consecutive elements of a row.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace lors {
+namespace {
+
+constexpr int NT = 256;
+constexpr unsigned long long kNoBad = ~0ull;
+
+// Reads the 32 "kept" flags of word w of row i (columns 32w .. 32w+31, those
+// at or past C read as not kept).  Source is either a dense uint8 mask or a
+// weight matrix (kept = value != 0, with -0 counting as zero).
+struct DenseSrc {
+    const uint8_t* p;
+    __device__ uint32_t flags(int64_t i, int C, int w) const {
+        const uint8_t* row = p + i * C;
+        const int c0 = w * 32;
+        uint32_t bits = 0;
+        if (c0 + 32 <= C && (((uintptr_t)(row + c0)) & 15) == 0) {
+            const u32x4 a = *(const u32x4*)(row + c0);
+            const u32x4 b = *(const u32x4*)(row + c0 + 16);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t v = q < 4 ? a[q] : b[q - 4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) bits |= (((v >> (8 * e)) & 0xFFu) != 0u ? 1u : 0u) << (4 * q + e);
+            }
+        } else {
+            for (int e = 0; e < 32 && c0 + e < C; ++e) bits |= (row[c0 + e] != 0 ? 1u : 0u) << e;
+        }
+        return bits;
+    }
+};
+
+struct Bf16WeightSrc {
+    const uint16_t* p;
+    __device__ uint32_t flags(int64_t i, int C, int w) const {
+        const uint16_t* row = p + i * C;
+        const int c0 = w * 32;
+        uint32_t bits = 0;
+        for (int e = 0; e < 32 && c0 + e < C; ++e) bits |= ((row[c0 + e] & 0x7FFFu) != 0u ? 1u : 0u) << e;
+        return bits;
+    }
+};
+
+struct F32WeightSrc {
+    const float* p;
+    __device__ uint32_t flags(int64_t i, int C, int w) const {
+        const float* row = p + i * C;
+        const int c0 = w * 32;
+        uint32_t bits = 0;
+        for (int e = 0; e < 32 && c0 + e < C; ++e) bits |= (row[c0 + e] != 0.f ? 1u : 0u) << e;
+        return bits;
+    }
+};
+
+template <class Src>
+__global__ __launch_bounds__(NT) void pack_bitmap_kernel(Src src, int64_t R, int C, int wpr,
+                                                         uint32_t* __restrict__ out) {
+    const int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (t >= R * wpr) return;
+    const int64_t i = t / wpr;
+    const int w = (int)(t - i * wpr);
+    out[t] = src.flags(i, C, w);
+}
+
+template <class Src>
+__global__ __launch_bounds__(NT) void pack_2_4_kernel(Src src, int64_t R, int C, int wpr,
+                                                      uint32_t* __restrict__ out,
+                                                      unsigned long long* __restrict__ first_bad) {
+    const int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (t >= R * wpr) return;
+    const int64_t i = t / wpr;
+    const int w = (int)(t - i * wpr);
+    const uint32_t f = src.flags(i, C, w);
+    uint32_t word = 0;
+    const int groups = C / 4;
+    for (int n = 0; n < 8; ++n) {
+        const int g = w * 8 + n;
+        if (g >= groups) break;
+        const uint32_t nib = (f >> (4 * n)) & 0xFu;
+        if (__popc(nib) != 2) {
+            atomicMin(first_bad, (unsigned long long)(i * groups + g));
+            continue;
+        }
+        const uint32_t p0 = __ffs(nib) - 1;
+        const uint32_t p1 = 31 - __clz(nib);
+        word |= (p0 | (p1 << 2)) << (4 * n);
+    }
+    out[t] = word;
+}
+
+__global__ void set_u64_kernel(unsigned long long* p, unsigned long long v) { *p = v; }
+
+__global__ void finish_first_bad_kernel(unsigned long long* p) {
+    if (*p == kNoBad) *(long long*)p = -1;
+}
+
+template <bool TWO_FOUR>
+__global__ __launch_bounds__(NT) void unpack_kernel(const uint32_t* __restrict__ in, int64_t R, int C,
+                                                    int wpr, uint8_t* __restrict__ dense) {
+    const int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (t >= R * wpr) return;
+    const int64_t i = t / wpr;
+    const int w = (int)(t - i * wpr);
+    const uint32_t word = in[t];
+    uint8_t* row = dense + i * C;
+    const int c0 = w * 32;
+    for (int e = 0; e < 32 && c0 + e < C; ++e) row[c0 + e] = (uint8_t)keep1<TWO_FOUR>(word, (uint32_t)e);
+}
+
+__global__ __launch_bounds__(NT) void zero_kernel(float* __restrict__ p, int64_t n) {
+    for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < n; t += (int64_t)gridDim.x * NT) p[t] = 0.f;
+}
+
+__global__ __launch_bounds__(NT) void zero2_kernel(float* __restrict__ a, int64_t na, float* __restrict__ b,
+                                                   int64_t nb) {
+    const int64_t stride = (int64_t)gridDim.x * NT;
+    for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < na + nb; t += stride) {
+        if (t < na) a[t] = 0.f;
+        else b[t - na] = 0.f;
+    }
+}
+
+// dbias[R] = column sums of dY[L x R]; thread owns one column and a slice of
+// rows, partial sums are combined with fp32 atomics (dbias zeroed first).
+template <bool BF16>
+__global__ __launch_bounds__(NT) void dbias_kernel(const void* __restrict__ dY, int64_t L, int R,
+                                                   int64_t rows_per_block, float* __restrict__ dbias) {
+    const int col = blockIdx.x * NT + threadIdx.x;
+    if (col >= R) return;
+    const int64_t l0 = (int64_t)blockIdx.y * rows_per_block;
+    const int64_t l1 = min(L, l0 + rows_per_block);
+    float acc = 0.f;
+    for (int64_t l = l0; l < l1; ++l) {
+        if constexpr (BF16)
+            acc += bf16_bits_to_f32(((const uint16_t*)dY)[l * R + col]);
+        else
+            acc += ((const float*)dY)[l * R + col];
+    }
+    atomicAdd(dbias + col, acc);
+}
+
+template <class Src>
+hipError_t launch_pack(Src src, int64_t R, int64_t C, bool two_four, uint32_t* packed,
+                       int64_t* first_bad, hipStream_t st) {
+    const int wpr = (int)((C + 31) / 32);
+    const int64_t n = R * wpr;
+    const unsigned blocks = (unsigned)((n + NT - 1) / NT);
+    if (two_four) {
+        auto* fb = (unsigned long long*)first_bad;
+        hipLaunchKernelGGL(set_u64_kernel, dim3(1), dim3(1), 0, st, fb, kNoBad);
+        if (n > 0)
+            hipLaunchKernelGGL(pack_2_4_kernel<Src>, dim3(blocks), dim3(NT), 0, st, src, R, (int)C, wpr,
+                               packed, fb);
+        hipLaunchKernelGGL(finish_first_bad_kernel, dim3(1), dim3(1), 0, st, fb);
+    } else {
+        if (first_bad)
+            hipLaunchKernelGGL(set_u64_kernel, dim3(1), dim3(1), 0, st, (unsigned long long*)first_bad,
+                               ~0ull);  // -1
+        if (n > 0)
+            hipLaunchKernelGGL(pack_bitmap_kernel<Src>, dim3(blocks), dim3(NT), 0, st, src, R, (int)C, wpr,
+                               packed);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_mask_pack(const uint8_t* dense, int64_t R, int64_t C, bool two_four,
+                            uint32_t* packed, int64_t* first_bad, hipStream_t st) {
+    return launch_pack(DenseSrc{dense}, R, C, two_four, packed, first_bad, st);
+}
+
+hipError_t launch_mask_from_weight(const void* W, bool w_is_bf16, int64_t R, int64_t C, bool two_four,
+                                   uint32_t* packed, int64_t* first_bad, hipStream_t st) {
+    if (w_is_bf16) return launch_pack(Bf16WeightSrc{(const uint16_t*)W}, R, C, two_four, packed, first_bad, st);
+    return launch_pack(F32WeightSrc{(const float*)W}, R, C, two_four, packed, first_bad, st);
+}
+
+hipError_t launch_mask_unpack(const uint32_t* packed, int64_t R, int64_t C, bool two_four, uint8_t* dense,
+                              hipStream_t st) {
+    const int wpr = (int)((C + 31) / 32);
+    const int64_t n = R * wpr;
+    if (n == 0) return hipSuccess;
+    const unsigned blocks = (unsigned)((n + NT - 1) / NT);
+    if (two_four)
+        hipLaunchKernelGGL(unpack_kernel<true>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, dense);
+    else
+        hipLaunchKernelGGL(unpack_kernel<false>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, dense);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    const int64_t want = (n + NT - 1) / NT;
+    const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
+    hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(NT), 0, st, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero2_f32(float* a, int64_t na, float* b, int64_t nb, hipStream_t st) {
+    const int64_t n = na + nb;
+    if (n == 0) return hipSuccess;
+    const int64_t want = (n + NT - 1) / NT;
+    const unsigned blocks = (unsigned)(want < 2048 ? want : 2048);
+    hipLaunchKernelGGL(zero2_kernel, dim3(blocks), dim3(NT), 0, st, a, na, b, nb);
+    return hipGetLastError();
+}
+
+static hipError_t launch_dbias(const LayerArgs& a, hipStream_t st, bool bf16) {
+    if (a.dbias == nullptr) return hipSuccess;
+    hipError_t e = launch_zero_f32(a.dbias, a.R, st);
+    if (e != hipSuccess || a.L == 0) return e;
+    int64_t ychunks = (a.L + 255) / 256;
+    if (ychunks > 4096) ychunks = 4096;
+    const int64_t rows = (a.L + ychunks - 1) / ychunks;
+    dim3 grid((unsigned)((a.R + NT - 1) / NT), (unsigned)ychunks), block(NT);
+    if (bf16)
+        hipLaunchKernelGGL(dbias_kernel<true>, grid, block, 0, st, a.dY, a.L, (int)a.R, rows, a.dbias);
+    else
+        hipLaunchKernelGGL(dbias_kernel<false>, grid, block, 0, st, a.dY, a.L, (int)a.R, rows, a.dbias);
+    return hipGetLastError();
+}
+
+hipError_t launch_dbias_bf16(const LayerArgs& a, hipStream_t st) { return launch_dbias(a, st, true); }
+hipError_t launch_dbias_f32(const LayerArgs& a, hipStream_t st) { return launch_dbias(a, st, false); }
+
+}  // namespace lors

@@ -1,0 +1,224 @@
+"""CPU tests of the C ABI: the library loads, exports every declared symbol,
+validates arguments in the documented order before touching the GPU, and its
+host mask packer matches the oracle's bit layout.
+
+No test here launches device work: every forward/backward call below is
+invalid and must be rejected on the host (fake but aligned addresses are
+used only in calls that validation refuses).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import masks as omasks
+from paper_2501_08582_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lors.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("liblors.so is not built (python -m paper_2501_08582_amd.build)")
+    return _lib.lib()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lors_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) == set(_lib.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code in range(11):
+        s = _lib.string(code)
+        assert s.startswith("LORS_")
+    assert "unknown" in _lib.string(99)
+    assert lib.lors_version() == 10000
+
+
+@pytest.mark.parametrize("R,C", [(1, 1), (3, 31), (3, 32), (5, 33), (4096, 14336)])
+def test_packed_bytes(lib, R, C):
+    assert _lib.mask_packed_bytes(R, C) == 4 * R * ((C + 31) // 32)
+
+
+# ---------------------------------------------------------------------------
+# host packer vs the oracle's layout
+# ---------------------------------------------------------------------------
+def _host_pack(M, fmt):
+    M = np.ascontiguousarray(M, dtype=np.uint8)
+    R, C = M.shape
+    out = np.zeros(R * ((C + 31) // 32), np.uint32)
+    bad = ctypes.c_int64(7)
+    st = _lib.mask_pack_host(M.ctypes.data, R, C, fmt, out.ctypes.data, ctypes.addressof(bad))
+    return st, out, bad.value
+
+
+def _host_unpack(words, R, C, fmt):
+    dense = np.zeros((R, C), np.uint8)
+    st = _lib.mask_unpack_host(np.ascontiguousarray(words).ctypes.data, R, C, fmt, dense.ctypes.data)
+    assert st == _lib.OK
+    return dense
+
+
+@pytest.mark.parametrize("C", [1, 8, 31, 32, 40, 100, 4096])
+def test_host_bitmap_matches_oracle(lib, C):
+    rng = np.random.default_rng(C)
+    M = (rng.random((9, C)) < 0.4).astype(np.uint8) * rng.integers(1, 255, (9, C)).astype(np.uint8)
+    st, out, bad = _host_pack(M, _lib.MASK_BITMAP)
+    assert st == _lib.OK and bad == -1
+    ref = omasks.pack_bitmap(M != 0)
+    assert np.array_equal(out, ref)
+    assert np.array_equal(_host_unpack(out, 9, C, _lib.MASK_BITMAP), (M != 0).astype(np.uint8))
+
+
+def _two_four(rng, R, C):
+    M = np.zeros((R, C), np.uint8)
+    for i in range(R):
+        for g in range(C // 4):
+            M[i, 4 * g + rng.choice(4, 2, replace=False)] = 1
+    return M
+
+
+@pytest.mark.parametrize("C", [4, 12, 32, 36, 64, 4096])
+def test_host_2_4_matches_oracle(lib, C):
+    rng = np.random.default_rng(C + 1)
+    M = _two_four(rng, 7, C)
+    st, out, bad = _host_pack(M, _lib.MASK_2_4)
+    assert st == _lib.OK and bad == -1
+    assert np.array_equal(out, omasks.pack_2_4(M))
+    assert np.array_equal(_host_unpack(out, 7, C, _lib.MASK_2_4), M)
+
+
+def test_host_2_4_rejects(lib):
+    rng = np.random.default_rng(5)
+    M = _two_four(rng, 4, 16)
+    M[2, 9] ^= 1  # row 2, group 2 now keeps 1 or 3
+    st, _, bad = _host_pack(M, _lib.MASK_2_4)
+    assert st == _lib.ERR_NOT_2_4
+    assert bad == omasks.first_bad_group_2_4(M) == 2 * 4 + 2
+
+
+def test_host_layout_fixture(lib):
+    # the same hand-derived words the oracle is pinned to
+    M = np.zeros((2, 40), np.uint8)
+    M[0, [0, 1, 5, 31, 32, 39]] = 1
+    M[1, [3, 16, 33]] = 1
+    st, out, _ = _host_pack(M, _lib.MASK_BITMAP)
+    assert st == _lib.OK
+    assert [hex(w) for w in out] == [hex(w) for w in (0x80000023, 0x81, 0x00010008, 0x2)]
+
+
+# ---------------------------------------------------------------------------
+# validation order and codes (all calls rejected before any HIP call)
+# ---------------------------------------------------------------------------
+BASE = 1 << 40  # fake, 16-byte aligned, far apart
+GAP = 1 << 34
+
+
+def _ptrs(n):
+    return [BASE + i * GAP for i in range(n)]
+
+
+def _fwd(p, ptrs, bias=None, ws_bytes=0):
+    X, W, M, B, A, Y = ptrs
+    return _lib.forward(p, X, W, M, B, A, bias, Y, None, ws_bytes, None)
+
+
+def _bwd(p, ptrs, dX="auto", dbias=None):
+    dY, X, W, M, B, A, dXp, dB, dA = ptrs
+    if dX == "auto":
+        dX = dXp
+    return _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, dbias, None, 0, None)
+
+
+def _p(**kw):
+    d = dict(R=64, C=64, L=32, r=8, scale=2.0, dtype=_lib.DTYPE_BF16, mask_format=_lib.MASK_BITMAP)
+    d.update(kw)
+    return _lib.problem(**d)
+
+
+def test_null_first(lib):
+    ptrs = _ptrs(6)
+    for k in range(6):
+        bad = list(ptrs)
+        bad[k] = None
+        # null wins over a bad dtype
+        assert _fwd(_p(dtype=9), bad) == _lib.ERR_NULL
+    st = _lib.lib().lors_forward(None, *_ptrs(5), None, BASE, None, 0, None)
+    assert st == _lib.ERR_NULL
+    bp = _ptrs(9)
+    for k in [0, 1, 2, 3, 4, 5, 7, 8]:
+        bad = list(bp)
+        bad[k] = None
+        assert _bwd(_p(), bad) == _lib.ERR_NULL
+
+
+def test_dtype_and_format(lib):
+    assert _fwd(_p(dtype=2), _ptrs(6)) == _lib.ERR_DTYPE
+    assert _fwd(_p(mask_format=5), _ptrs(6)) == _lib.ERR_MASK_FORMAT
+    assert _fwd(_p(mask_format=_lib.MASK_2_4, C=66), _ptrs(6)) == _lib.ERR_MASK_FORMAT
+
+
+@pytest.mark.parametrize("kw", [dict(R=0), dict(C=0), dict(L=-1), dict(r=0), dict(r=129),
+                                dict(R=1 << 31), dict(scale=float("inf")), dict(scale=float("nan"))])
+def test_shape(lib, kw):
+    assert _fwd(_p(**kw), _ptrs(6)) == _lib.ERR_SHAPE
+
+
+@pytest.mark.parametrize("kw", [dict(R=60), dict(C=36), dict(dtype=_lib.DTYPE_F32, C=66),
+                                dict(flags=_lib.FLAG_BWD_STE)])
+def test_unsupported(lib, kw):
+    assert _fwd(_p(**kw), _ptrs(6)) == _lib.ERR_UNSUPPORTED
+
+
+def test_alignment(lib):
+    for k in range(6):
+        bad = _ptrs(6)
+        bad[k] += 8
+        assert _fwd(_p(), bad) == _lib.ERR_ALIGN
+    assert _fwd(_p(), _ptrs(6), bias=BASE + 7 * GAP + 4) == _lib.ERR_ALIGN
+
+
+def test_alias(lib):
+    ptrs = _ptrs(6)
+    ptrs[5] = ptrs[0] + 16  # Y overlaps X
+    assert _fwd(_p(), ptrs) == _lib.ERR_ALIAS
+    ptrs = _ptrs(6)
+    assert _fwd(_p(), ptrs, bias=ptrs[5] + 64) == _lib.ERR_ALIAS  # bias inside Y
+    bp = _ptrs(9)
+    bp[8] = bp[7] + 16  # dA overlaps dB
+    assert _bwd(_p(), bp) == _lib.ERR_ALIAS
+    bp = _ptrs(9)
+    bp[6] = bp[0]  # dX == dY
+    assert _bwd(_p(), bp) == _lib.ERR_ALIAS
+
+
+def test_workspace_query(lib):
+    assert _lib.workspace_bytes(_p()) == 0
+    assert _lib.workspace_bytes(_p(R=0)) == 2**64 - 1
+
+
+def test_mask_entry_validation(lib):
+    L = _lib.lib()
+    assert L.lors_mask_pack(None, 4, 4, 0, BASE, None, None) == _lib.ERR_NULL
+    assert L.lors_mask_pack(BASE, 4, 8, 1, BASE + GAP, None, None) == _lib.ERR_NULL  # 2:4 needs first_bad
+    assert L.lors_mask_pack(BASE, 4, 6, 1, BASE + GAP, BASE + 2 * GAP, None) == _lib.ERR_MASK_FORMAT
+    assert L.lors_mask_pack(BASE, 4, 8, 3, BASE + GAP, None, None) == _lib.ERR_MASK_FORMAT
+    assert L.lors_mask_pack(BASE, -1, 8, 0, BASE + GAP, None, None) == _lib.ERR_SHAPE
+    assert L.lors_mask_pack(BASE + 1, 4, 8, 0, BASE + GAP, None, None) == _lib.ERR_ALIGN
+    assert L.lors_mask_pack(BASE, 4, 64, 0, BASE + 16, None, None) == _lib.ERR_ALIAS
+    assert L.lors_mask_unpack(BASE, 4, 64, 0, BASE + 16, None) == _lib.ERR_ALIAS
+    assert L.lors_mask_from_weight(BASE, 7, 4, 8, 0, BASE + GAP, None, None) == _lib.ERR_DTYPE
+    assert L.lors_mask_pack_host(None, 2, 2, 0, None, None) == _lib.ERR_NULL
