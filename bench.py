@@ -60,9 +60,9 @@ def cpu_baseline(inp, args):
 
     wl = inp.wl
     f = obf16.to_f64 if wl.dtype == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
-    # Bounded sample: the full weight with a slice of the tokens, sized so one
-    # oracle pass is a few seconds; repeated until --cpu-seconds have passed.
-    Ls = min(wl.L, 1024)
+    # Bounded sample: one full forward+backward of the layer, repeated until
+    # --cpu-seconds have passed (best pass reported).
+    Ls = wl.L
     X, dY = f(inp.X[:Ls]), f(inp.dY[:Ls])
     W, B, A = f(inp.W), f(inp.B), f(inp.A)
     best, n, t_all = None, 0, time.perf_counter()
@@ -83,7 +83,7 @@ def cpu_baseline(inp, args):
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"{wl.name}: full {wl.R}x{wl.C} weight, r={wl.r}, first {Ls} of {wl.L} tokens; "
+        "sample": (f"{wl.name}: {wl.R}x{wl.C} weight, r={wl.r}, {Ls} of {wl.L} tokens; "
                    f"numpy fp64 forward+backward, best of {n} passes ({best:.2f} s each)"),
     }
 
