@@ -5,33 +5,38 @@
 //
 // (I_w^4, I_w^5 and the two adapter gradients of the SP-LoRA backward list in
 // Section 2.2, with the scale of the listing.)  The weight-gradient GEMM runs
-// over K = L with both operands token-major, so each K-step transposes its dY
-// and X tiles into LDS.  After the K loop the fp32 accumulators are masked in
-// registers, rounded to bf16, and fed to two rank-r MFMA products whose
-// per-tile partial sums are added into dB and dA with fp32 atomics (dB and dA
-// must be zero on entry).
-#include "device_common.hpp"
+// over K = L with both operands token-major: each K-step copies a 64-token
+// slab of dY and of X straight from HBM into LDS in natural layout, and the
+// MFMA operands are read back with the LDS transpose load, so no lane ever
+// shuffles data.  Four waves each own a 128 x 128 block of the 256 x 256 G
+// tile (fp32 accumulators in AGPRs); LDS is double-buffered.
+//
+// Epilogue: the accumulators are masked in registers and rounded to bf16.
+// dA uses them directly as the MFMA B operand (contraction over the rows of G
+// in the accumulator's own row order); dB reads G^T back from LDS.  Per-tile
+// partial sums are added into dB and dA with fp32 atomics, so dB and dA must
+// be zero on entry.
+#include "gemm_common.hpp"
 #include "kernels.hpp"
 
 namespace lors {
 namespace {
 
+constexpr int NT = 256;
 constexpr int BM = 256;  // rows of G (output features, R) per tile
 constexpr int BN = 256;  // columns of G (input features, C) per tile
 constexpr int BK = 64;   // tokens per K-step
-constexpr int NT = 512;
-constexpr int WM = 2, WN = 4;
-constexpr int FM = BM / WM / 32;
-constexpr int FN = BN / WN / 32;
-constexpr int LDT = BK + 8;   // pitch of the transposed tiles [i][l] and [j][l]
-constexpr int LDG = BN + 8;   // pitch of the bf16 G tile [i][j]
+constexpr int TILEB = BK * kRowBytes;  // 32 KiB: one operand slab
+constexpr int STAGEB = 2 * TILEB;      // dY slab + X slab
+constexpr int SMEM = 2 * STAGEB;       // two stages
 constexpr int GROUP_M = 4;
+constexpr int LOADS = TILEB / 1024 / (NT / kWave);  // 1 KiB copies per wave per slab (8)
 
-constexpr int kMainBytes = (BM + BN) * LDT * 2;
-constexpr int kGBytes = BM * LDG * 2;
-constexpr int kSmemBytes = kMainBytes > kGBytes ? kMainBytes : kGBytes;
-
-static_assert(BM / 32 == NT / kWave, "one dB row block per wave");
+// Epilogue LDS carve-up (reuses the stage buffers).
+constexpr int GT_PITCH = 512;                      // G^T tile: [j][i], 256 i per row
+constexpr int GT_BYTES = BN * GT_PITCH;            // 128 KiB
+constexpr int MASK_OFF = 0;                        // mask tile [i][8 words] (before G^T)
+constexpr int BT_PITCH = BM + 8;                   // B^T tile [j'][i], elements per row
 
 template <int RK, bool TWO_FOUR>
 __global__ __launch_bounds__(NT, 1) void g_kernel(
@@ -39,20 +44,17 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, float* __restrict__ dB, float* __restrict__ dA,
     int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n) {
-    constexpr int JB = (RK + 1) / 2;         // 32-wide blocks of the rank
-    constexpr int LDB = BM + 8;              // pitch of B^T [j][i]
-    static_assert(JB * 32 * LDB * 2 <= kSmemBytes, "B^T fits");
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kSmemBytes];
-    uint16_t* Dt = (uint16_t*)smem;                    // [i][l]
-    uint16_t* Xt = (uint16_t*)(smem + BM * LDT * 2);   // [j][l]
-    uint16_t* Gs = (uint16_t*)smem;                    // [i][j], epilogue
-    uint16_t* Bt = (uint16_t*)smem;                    // [j'][i], epilogue
+    constexpr int JB = (RK + 1) / 2;  // 32-wide blocks of the rank
+    static_assert(GT_BYTES <= SMEM, "G^T tile fits");
+    static_assert(JB * 32 * BT_PITCH * 2 <= SMEM, "B^T tile fits");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31;
     const int h = lane >> 5;
+    const int wi = wave >> 1, wj = wave & 1;
 
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, tm, tn);
@@ -61,112 +63,160 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const int64_t nk = (L + BK - 1) / BK;
     const int wpr = (C + 31) >> 5;
 
-    // K-step staging: thread t loads rows 4*(t/32) .. +3 of the token block and
-    // 8 consecutive columns starting at 8*(t%32), for dY (columns = R) and X
-    // (columns = C), then writes them transposed, four tokens per 8-byte store.
-    const int cq = tid & 31;
-    const int rg = tid >> 5;
-    u32x4 dr[4], xr[4];
-
-    auto load_tiles = [&](int64_t kt) {
-        const int64_t l0 = kt * BK + 4 * rg;
+    // ---- asynchronous slab copies: copy q of this wave fills tile rows
+    // 2*(8*wave + q) + {0, 1}; lane l covers physical chunk l % 32 of its row.
+    const int pchunk = lane & 31;
+    const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+    auto issue = [&](int64_t kt, int st) {
+        const uint32_t sb = lds0 + st * STAGEB;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t gl = l0 + q;
-            const int gi = i0 + cq * 8, gj = j0 + cq * 8;
-            dr[q] = (gl < L && gi < R) ? *(const u32x4*)(dY + gl * R + gi) : zero_u32x4();
-            xr[q] = (gl < L && gj < C) ? *(const u32x4*)(X + gl * C + gj) : zero_u32x4();
+        for (int q = 0; q < LOADS; ++q) {
+            const int row = 2 * (LOADS * wave + q) + h;
+            const int lc = swz_chunk(row, pchunk);
+            const int64_t gl = kt * BK + row;
+            const int gi = i0 + lc * 8, gj = j0 + lc * 8;
+            const void* a = (gl < L && gi < R) ? (const void*)(dY + gl * R + gi) : (const void*)zsrc;
+            const void* b = (gl < L && gj < C) ? (const void*)(X + gl * C + gj) : (const void*)zsrc;
+            copy16_to_lds(a, sb + (LOADS * wave + q) * 1024);
+            copy16_to_lds(b, sb + TILEB + (LOADS * wave + q) * 1024);
         }
     };
 
-    auto store_transposed = [&](uint16_t* dst, const u32x4* v) {
+    // Per-lane fragment offsets inside a slab (stage and chunk added later).
+    int offA[4][2], offB[4][2];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int sh = (e & 1) * 16;
-            const int w = e >> 1;
-            u32x2 o;
-            o[0] = ((v[0][w] >> sh) & 0xFFFFu) | (((v[1][w] >> sh) & 0xFFFFu) << 16);
-            o[1] = ((v[2][w] >> sh) & 0xFFFFu) | (((v[3][w] >> sh) & 0xFFFFu) << 16);
-            *(u32x2*)(dst + (cq * 8 + e) * LDT + 4 * rg) = o;
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            offA[b][t] = tr_frag_off(lane, 0, wi * 128 + 32 * b, t);
+            offB[b][t] = TILEB + tr_frag_off(lane, 0, wj * 128 + 32 * b, t);
         }
-    };
 
-    f32x16 acc[FM][FN];
+    f32x16 acc[4][4];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int b = 0; b < 4; ++b)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
 
-    const int wm = wave / WN, wn = wave % WN;
-
-    if (nk > 0) load_tiles(0);
+    if (nk > 0) issue(0, 0);
+    if (nk > 1) issue(1, 1);
     for (int64_t kt = 0; kt < nk; ++kt) {
-        __syncthreads();
-        store_transposed(Dt, dr);
-        store_transposed(Xt, xr);
-        __syncthreads();
-        if (kt + 1 < nk) load_tiles(kt + 1);
+        const int st = (int)(kt & 1);
+        if (kt + 1 < nk)
+            stage_barrier<2 * LOADS>();  // this stage landed; the next may still fly
+        else
+            stage_barrier<0>();
+        const uint8_t* sb = smem + st * STAGEB;
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8 a[FM], b[FN];
+        for (int c = 0; c < BK / 16; ++c) {
+            const int rowoff = 16 * c * kRowBytes;  // 16 rows further (swizzle period 4 divides 16)
+            bf16x8 fa[4], fb[4];
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                a[i] = *(const bf16x8*)(Dt + (wm * (BM / WM) + 32 * i + l32) * LDT + 16 * ks + 8 * h);
+            for (int b = 0; b < 4; ++b) {
+                fa[b] = frag_from_tr(lds_tr_read(sb + rowoff + offA[b][0]), lds_tr_read(sb + rowoff + offA[b][1]));
+                fb[b] = frag_from_tr(lds_tr_read(sb + rowoff + offB[b][0]), lds_tr_read(sb + rowoff + offB[b][1]));
+            }
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                b[j] = *(const bf16x8*)(Xt + (wn * (BN / WN) + 32 * j + l32) * LDT + 16 * ks + 8 * h);
+            for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(a[i], b[j], acc[i][j]);
+                for (int b = 0; b < 4; ++b) acc[a][b] = mfma_32x32x16(fa[a], fb[b], acc[a][b]);
         }
+        lds_barrier();  // every wave is done reading this stage
+        if (kt + 2 < nk) issue(kt + 2, st);
     }
+    stage_barrier<0>();
 
-    // ---- epilogue 1: mask in registers, round to bf16, keep in acc, and
-    // write the bf16 G tile to LDS as [i][j].
+    // ---- epilogue 1: mask words of the tile -> LDS as [i][8 words].
+    uint32_t* msk = (uint32_t*)(smem + MASK_OFF);
+    for (int e = tid; e < BM * 8; e += NT) {
+        const int il = e >> 3, w = e & 7;
+        const int gi = i0 + il, gw = (j0 >> 5) + w;
+        msk[e] = (gi < R && gw < wpr) ? Mp[(int64_t)gi * wpr + gw] : 0u;
+    }
     __syncthreads();
+
+    // ---- epilogue 2: select by the mask, round to bf16, keep the packed
+    // fragments: gb[a][b][c] holds accumulator elements 8c .. 8c+7 of block
+    // (a, b) (rows 16c + 4h + {0..3} and 16c + 8 + 4h + {0..3}).
+    u32x4 gb[4][4][2];
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int jl = wn * (BN / WN) + 32 * j + l32;
-        const int gj = j0 + jl;
-        const int wcol = gj >> 5;
+    for (int a = 0; a < 4; ++a) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
+        for (int v4 = 0; v4 < 4; ++v4) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int il = wm * (BM / WM) + 32 * i + 8 * (v >> 2) + 4 * h + (v & 3);
-                const int gi = i0 + il;
-                const uint32_t word = (gi < R && gj < C) ? Mp[(int64_t)gi * wpr + wcol] : 0u;
-                const float g = keep1<TWO_FOUR>(word, (uint32_t)(gj & 31)) ? acc[i][j][v] : 0.f;
-                const uint16_t gb = bf16_bits(g);
-                acc[i][j][v] = bf16_bits_to_f32(gb);
-                Gs[il * LDG + jl] = gb;
+            for (int q = 0; q < 4; ++q) {
+                const int il = wi * 128 + 32 * a + 8 * v4 + 4 * h + q;
+                const u32x4 words = *(const u32x4*)(msk + il * 8 + wj * 4);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const uint32_t keep = keep1<TWO_FOUR>(words[b], (uint32_t)l32);
+                    acc[a][b][4 * v4 + q] = keep ? acc[a][b][4 * v4 + q] : 0.f;
+                }
             }
         }
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    gb[a][b][c][e] = pack_bf16x2(acc[a][b][8 * c + 2 * e], acc[a][b][8 * c + 2 * e + 1]);
     }
+    __syncthreads();  // mask tile no longer needed
+
+    // ---- epilogue 3: G^T -> LDS as [j][i] (pitch 512 B; the quad of 16-byte
+    // chunks is XORed with j % 8 so that transpose reads of 4 consecutive j
+    // hit different banks).  Lane (j, h) stores rows 8*v4 + 4h + {0..3}.
+    auto gt_off = [](int j, int i) {
+        return j * GT_PITCH + (((i >> 3) ^ ((j & 7) << 2)) << 4) + ((i & 7) << 1);
+    };
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int jl = wj * 128 + 32 * b + l32;
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+                const int il = wi * 128 + 32 * a + 8 * v4 + 4 * h;
+                const u32x4& g = gb[a][b][v4 >> 1];
+                u32x2 o;
+                o[0] = g[2 * (v4 & 1)];
+                o[1] = g[2 * (v4 & 1) + 1];
+                *(u32x2*)(smem + gt_off(jl, il)) = o;
+            }
+        }
     __syncthreads();
 
-    // ---- epilogue 2: dB[i][j'] += s * sum_j G[i][j] A[j'][j]; wave w owns
-    // rows i = 32w .. 32w+31 of the tile, all 32-wide rank blocks.
-    {
+    // ---- epilogue 4: dB[i][j'] += s * sum_j G[i][j] A[j'][j].  Wave w owns
+    // tile rows 64w .. 64w+63.  A operand (rows i, 8 consecutive j) is read
+    // from G^T with the transpose load; B operand straight from A in HBM.
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib) {
+        const int irow0 = 64 * wave + 32 * ib;
         f32x16 db[JB];
 #pragma unroll
         for (int b = 0; b < JB; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) db[b][v] = 0.f;
-        const bool a_ok = true;
-        (void)a_ok;
-#pragma unroll 4
-        for (int ks = 0; ks < BN / 16; ++ks) {
-            const bf16x8 ga = *(const bf16x8*)(Gs + (wave * 32 + l32) * LDG + 16 * ks + 8 * h);
-            const int gj = j0 + 16 * ks + 8 * h;
+        for (int kc = 0; kc < BN / 16; ++kc) {
+            // transpose read from the [j][i] tile: rows j, columns i
+            u32x2 lo, hi;
+            {
+                const int g = lane >> 4, jj = lane & 15;
+                const int jr0 = 16 * kc + 8 * (g >> 1) + (jj >> 2);
+                const int ic = irow0 + 16 * (g & 1) + 4 * (jj & 3);
+                lo = lds_tr_read(smem + gt_off(jr0, ic));
+                hi = lds_tr_read(smem + gt_off(jr0 + 4, ic));
+            }
+            const bf16x8 ga = frag_from_tr(lo, hi);
+            const int gj = j0 + 16 * kc + 8 * h;
 #pragma unroll
             for (int b = 0; b < JB; ++b) {
-                const int jr = 32 * b + l32;  // rank index j'
-                const u32x4 av = (jr < r && gj < C) ? *(const u32x4*)(Am + (int64_t)jr * C + gj)
-                                                   : zero_u32x4();
+                const int jr = 32 * b + l32;
+                const u32x4 av = (jr < r && gj < C) ? *(const u32x4*)(Am + (int64_t)jr * C + gj) : zero_u32x4();
                 db[b] = mfma_32x32x16(ga, as_bf16x8(av), db[b]);
             }
         }
@@ -176,53 +226,47 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
             if (jr >= r) continue;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int gi = i0 + wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+                const int gi = i0 + irow0 + 8 * (v >> 2) + 4 * h + (v & 3);
                 if (gi < R) atomicAdd(dB + (int64_t)gi * r + jr, s * db[b][v]);
             }
         }
     }
     __syncthreads();
 
-    // ---- epilogue 3: B^T of the tile's rows into LDS as [j'][i].
-    for (int c = tid; c < BM * JB * 32; c += NT) {
-        const int il = c / (JB * 32), jr = c % (JB * 32);
+    // ---- epilogue 5: B^T of the tile's rows -> LDS as [j'][i] (padded pitch).
+    uint16_t* bt = (uint16_t*)smem;
+    for (int e = tid; e < BM * JB * 32; e += NT) {
+        const int il = e / (JB * 32), jr = e % (JB * 32);
         const int gi = i0 + il;
-        Bt[jr * LDB + il] = (gi < R && jr < r) ? Bm[(int64_t)gi * r + jr] : (uint16_t)0;
+        bt[jr * BT_PITCH + il] = (gi < R && jr < r) ? Bm[(int64_t)gi * r + jr] : (uint16_t)0;
     }
     __syncthreads();
 
-    // ---- epilogue 4: dA[j'][j] += s * sum_i B[i][j'] G[i][j], straight from
-    // the masked accumulators.  For a 32-row block, MFMA K-chunk c uses
-    // accumulator elements 8c .. 8c+7, i.e. rows 16c + 4h + {0..3} and
-    // 16c + 8 + 4h + {0..3}; the B^T operand is read with the same row order.
+    // ---- epilogue 6: dA[j'][j] += s * sum_i B[i][j'] G[i][j] with the masked
+    // bf16 accumulators as the B operand (K = rows i in accumulator order).
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int gj = j0 + wn * (BN / WN) + 32 * j + l32;
+    for (int b = 0; b < 4; ++b) {
+        const int gj = j0 + wj * 128 + 32 * b + l32;
 #pragma unroll
-        for (int b = 0; b < JB; ++b) {
+        for (int jb = 0; jb < JB; ++jb) {
             f32x16 da;
 #pragma unroll
             for (int v = 0; v < 16; ++v) da[v] = 0.f;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int ib = wm * (BM / WM) + 32 * i;
+            for (int a = 0; a < 4; ++a) {
+                const int ib = wi * 128 + 32 * a;
 #pragma unroll
                 for (int c = 0; c < 2; ++c) {
-                    bf16x8 gb;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) gb[e] = (__bf16)acc[i][j][8 * c + e];
-                    const uint16_t* bt = Bt + (32 * b + l32) * LDB + ib + 16 * c + 4 * h;
-                    u32x4 bv;
-                    const u32x2 lo = *(const u32x2*)(bt);
-                    const u32x2 hi = *(const u32x2*)(bt + 8);
-                    bv[0] = lo[0]; bv[1] = lo[1]; bv[2] = hi[0]; bv[3] = hi[1];
-                    da = mfma_32x32x16(as_bf16x8(bv), gb, da);
+                    const uint16_t* p = bt + (32 * jb + l32) * BT_PITCH + ib + 16 * c + 4 * h;
+                    const u32x2 lo = *(const u32x2*)p;
+                    const u32x2 hi = *(const u32x2*)(p + 8);
+                    da = mfma_32x32x16(frag_from_tr(lo, hi), as_bf16x8(gb[a][b][c]), da);
                 }
             }
             if (gj < C) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int jr = 32 * b + 8 * (v >> 2) + 4 * h + (v & 3);
+                    const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
                     if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
                 }
             }
@@ -240,11 +284,11 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     auto* B = (const uint16_t*)a.B;
     auto* A = (const uint16_t*)a.A;
     if (a.two_four)
-        hipLaunchKernelGGL((g_kernel<RK, true>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((g_kernel<RK, true>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     else
-        hipLaunchKernelGGL((g_kernel<RK, false>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((g_kernel<RK, false>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
 }
 

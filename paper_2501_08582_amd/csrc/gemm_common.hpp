@@ -1,0 +1,105 @@
+// Building blocks of the 4-wave gfx950 GEMM main loops: asynchronous
+// global -> LDS copies, swizzled LDS tiles, and MFMA operand fragments read
+// with the gfx950 LDS transpose load.
+//
+// Tiles are stored in LDS in their natural row-major order (one 512-byte row =
+// 256 bf16) with the 16-byte chunks of row `row` permuted as
+// chunk ^ (4 * (row % 4)), so that the 4-row x 16-column blocks fetched by
+// ds_read_b64_tr_b16 hit 16 different bank groups per half wave.
+#pragma once
+
+#include "device_common.hpp"
+
+namespace lors {
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 1 KiB of zeros (one copy per code object): the source of every lane whose
+// tile element lies outside its tensor, so out-of-range parts of a tile read
+// as 0.  Never written.
+static __device__ __attribute__((aligned(1024))) uint32_t g_zero_page[256];
+
+constexpr int kRowBytes = 512;  // one tile row: 256 bf16
+
+__device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ ((row & 3) << 2); }
+
+// Byte offset of element (row, col) inside a swizzled 256-column tile.
+__device__ __forceinline__ int tile_off(int row, int col) {
+    return row * kRowBytes + (swz_chunk(row, col >> 3) << 4) + ((col & 7) << 1);
+}
+
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One 16-byte global -> LDS copy per lane (global_load_lds_dwordx4): lane l's
+// data lands at LDS byte address lds_wave_base + 16*l; lds_wave_base must be
+// wave-uniform.  Issued as inline assembly so that the compiler does not
+// serialise it against later LDS reads: completion is tracked explicitly with
+// vmcnt (see stage_barrier).
+// (M0 is written here and nowhere else in these kernels; one wait state
+// separates the M0 write from the LDS DMA that reads it.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_wave_base) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(lds_wave_base)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N of this wave's vector-memory loads (including the
+// LDS copies above) are outstanding, then barrier: afterwards every copy
+// issued before the last N of every wave is visible in LDS.
+template <int N>
+__device__ __forceinline__ void stage_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
+// Barrier after which LDS written or read before it may be reused.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+}
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane j supplies the
+// address of row j/4, columns 4*(j%4) .. +3 of a 4 x 16 block of 16-bit
+// values; lane i receives the 4 values of column i (rows 0..3).
+__device__ __forceinline__ u32x2 lds_tr_read(const uint8_t* p) {
+    i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+    return __builtin_bit_cast(u32x2, v);
+}
+
+// Byte offset, inside a swizzled tile whose rows are the MFMA K dimension,
+// of this lane's part of the transpose read `t` (0 or 1) that builds the
+// 32x32x16 operand of the 32 columns starting at col0 and the 16 rows
+// starting at row0.  Lane l ends up with rows row0 + 8*(l/32) + 4t + {0..3}
+// of column col0 + l%32, i.e. operand elements 4t .. 4t+3.
+__device__ __forceinline__ int tr_frag_off(int lane, int row0, int col0, int t) {
+    const int g = lane >> 4, j = lane & 15;
+    const int row = row0 + 8 * (g >> 1) + 4 * t + (j >> 2);
+    const int col = col0 + 16 * (g & 1) + 4 * (j & 3);
+    return tile_off(row, col);
+}
+
+__device__ __forceinline__ bf16x8 frag_from_tr(u32x2 lo, u32x2 hi) {
+    u32x4 v;
+    v[0] = lo[0];
+    v[1] = lo[1];
+    v[2] = hi[0];
+    v[3] = hi[1];
+    return as_bf16x8(v);
+}
+
+// s_waitcnt vmcnt(n) leaving the LDS/export counters unconstrained (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+}  // namespace lors
