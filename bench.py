@@ -116,8 +116,9 @@ def main():
     dA = torch.empty((r, C), dtype=torch.float32, device="cuda")
     p = _lib.problem(R, C, L, r, s, _lib.DTYPE_BF16 if dt == "bf16" else _lib.DTYPE_F32,
                      _lib.MASK_2_4 if fmt == ops.TWO_FOUR else _lib.MASK_BITMAP)
+    p_reuse = _lib.problem(R, C, L, r, s, p.dtype, p.mask_format, _lib.FLAG_REUSE_MASK_T)
     ws = _lib.workspace_bytes(p)
-    assert ws == 0, "the library needs no workspace for these problems"
+    wsbuf = torch.empty(max(ws, 1), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
     ptr = lambda t: t.data_ptr()  # noqa: E731
@@ -129,12 +130,14 @@ def main():
                    "lors_forward")
         if ev is not None:
             ev[1].record(stream)
-        _lib.check(_lib.backward_data(p, ptr(dY), ptr(W), ptr(M), ptr(B), ptr(A), ptr(dX), None, 0, sh),
-                   "lors_backward_data")
+        # the data half rebuilds the transposed mask in the workspace; the
+        # weight half of the same step reuses it
+        _lib.check(_lib.backward_data(p, ptr(dY), ptr(W), ptr(M), ptr(B), ptr(A), ptr(dX), ptr(wsbuf), ws,
+                                      sh), "lors_backward_data")
         if ev is not None:
             ev[2].record(stream)
-        _lib.check(_lib.backward_weight(p, ptr(dY), ptr(X), ptr(M), ptr(B), ptr(A), ptr(dB), ptr(dA),
-                                        None, None, 0, sh), "lors_backward_weight")
+        _lib.check(_lib.backward_weight(p_reuse, ptr(dY), ptr(X), ptr(M), ptr(B), ptr(A), ptr(dB), ptr(dA),
+                                        None, ptr(wsbuf), ws, sh), "lors_backward_weight")
         if ev is not None:
             ev[3].record(stream)
 
@@ -170,7 +173,8 @@ def main():
               "bwd_weight": costs.g_flops(R, C, L, r)}
     kbytes = costs.min_hbm_bytes(R, C, L, r, elt=2 if dt == "bf16" else 4)
     kbytes = {"fwd": kbytes["fwd"], "bwd_data": kbytes["dx"], "bwd_weight": kbytes["g"]}
-    kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel", "bwd_weight": "g_kernel (+ dA/dB clear)"}
+    kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel (+ mask transpose)",
+                    "bwd_weight": "g_kernel (+ dA/dB clear)"}
 
     flops = costs.algorithmic_flops(R, C, L, r)
     value = flops / (ms_step * 1e-3) / 1e12

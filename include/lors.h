@@ -100,12 +100,20 @@ typedef enum lors_mask_format {
  * (Algorithm 2).  Currently rejected with LORS_ERR_UNSUPPORTED. */
 #define LORS_FLAG_BWD_STE 0x1u
 
+/* Backward calls only: the workspace already holds the transposed mask that
+ * an earlier backward call wrote for the same M_packed, R and C (its
+ * contents were not touched since), so it is not rebuilt.  The mask of a
+ * sparse layer is frozen during fine-tuning, so a training loop can pass
+ * this flag from the second step on, or between lors_backward_data and
+ * lors_backward_weight of one step. */
+#define LORS_FLAG_REUSE_MASK_T 0x2u
+
 /*
  * Problem description.
  *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
  *   1 <= r <= 128, every extent < 2^31, scale finite.
- *   bf16: R % 8 == 0 and C % 8 == 0;  fp32: R % 4 == 0 and C % 4 == 0
- *   (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
+ *   bf16: R % 8 == 0, C % 8 == 0 and r % 8 == 0;  fp32: R % 4 == 0 and
+ *   C % 4 == 0 (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
  */
 typedef struct lors_problem {
     int64_t R;
@@ -115,7 +123,7 @@ typedef struct lors_problem {
     float scale;
     int32_t dtype;        /* lors_dtype_t */
     int32_t mask_format;  /* lors_mask_format_t */
-    uint32_t flags;       /* must be 0 */
+    uint32_t flags;       /* 0 or LORS_FLAG_REUSE_MASK_T */
 } lors_problem_t;
 
 /* Human-readable name of a status code (static storage). */
@@ -163,8 +171,12 @@ lors_status_t lors_mask_pack_host(const uint8_t* dense, int64_t R, int64_t C,
 lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C,
                                     int32_t mask_format, uint8_t* dense);
 
-/* Device scratch bytes lors_forward/lors_backward need for problem p
- * (currently 0 for every supported problem; (size_t)-1 if p is invalid). */
+/* Device scratch bytes the backward calls (lors_backward, lors_backward_data,
+ * lors_backward_weight) need for problem p: for bf16 the transposed bitmap of
+ * the mask, 4 * C * ceil(R/32) bytes rounded up to 256 (about R*C/8, i.e.
+ * 1/16 of W); 0 for fp32.  (size_t)-1 if p is invalid.  The workspace must be
+ * 16-byte aligned, must not overlap any argument, and is overwritten; its
+ * contents on return are unspecified.  lors_forward needs no workspace. */
 size_t lors_workspace_bytes(const lors_problem_t* p);
 
 /*

@@ -31,6 +31,7 @@ DTYPE_F32 = 1
 MASK_BITMAP = 0
 MASK_2_4 = 1
 FLAG_BWD_STE = 0x1
+FLAG_REUSE_MASK_T = 0x2
 
 EXPORTED = (
     "lors_status_string", "lors_version", "lors_mask_packed_bytes", "lors_mask_pack",

@@ -50,9 +50,11 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
     if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
     if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
-    if (p->flags != 0u) return LORS_ERR_UNSUPPORTED;
+    if ((p->flags & ~LORS_FLAG_REUSE_MASK_T) != 0u) return LORS_ERR_UNSUPPORTED;
     const int64_t row_align = p->dtype == LORS_DTYPE_BF16 ? 8 : 4;
     if (p->R % row_align != 0 || p->C % row_align != 0) return LORS_ERR_UNSUPPORTED;
+    // bf16: rows of B are copied and read 16 bytes at a time.
+    if (p->dtype == LORS_DTYPE_BF16 && p->r % 8 != 0) return LORS_ERR_UNSUPPORTED;
     if (p->dtype == LORS_DTYPE_F32) {
         // The fp32 kernels put token tiles of 64 on the second grid axis.
         if ((p->L + 63) / 64 > 65535 || (p->R + 63) / 64 > 65535) return LORS_ERR_UNSUPPORTED;
@@ -95,9 +97,13 @@ size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
     return static_cast<size_t>(R * words_per_row(C) * 4);
 }
 
+// bf16 backward: the transposed bitmap M^T (C rows of ceil(R/32) words),
+// rounded up to 256 bytes.  The forward and the fp32 path need nothing.
 size_t lors_workspace_bytes(const lors_problem_t* p) {
     if (p == nullptr || check_problem(p) != LORS_OK) return static_cast<size_t>(-1);
-    return 0;
+    if (p->dtype != LORS_DTYPE_BF16) return 0;
+    const int64_t bytes = p->C * ((p->R + 31) / 32) * 4;
+    return static_cast<size_t>((bytes + 255) / 256 * 256);
 }
 
 // ---------------------------------------------------------------------------
@@ -240,8 +246,8 @@ lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W
                          bias ? range_of(bias, R * es) : Range{0, 0}};
     for (const Range& in : ins)
         if (overlap(y, in)) return LORS_ERR_ALIAS;
-    if (workspace_bytes < lors_workspace_bytes(p)) return LORS_ERR_WORKSPACE;
-    (void)workspace;
+    (void)workspace;  // the forward needs no scratch
+    (void)workspace_bytes;
 
     lors::LayerArgs a{};
     a.R = R; a.C = C; a.L = L; a.r = r;
@@ -258,10 +264,11 @@ namespace {
 // optional outputs have been mapped to nullptr by the caller.
 lors_status_t check_backward(const lors_problem_t* p, const void* dY, const void* X, const void* W,
                              const uint32_t* M_packed, const void* B, const void* A, void* dX, float* dB,
-                             float* dA, float* dbias, size_t workspace_bytes) {
+                             float* dA, float* dbias, const void* workspace, size_t workspace_bytes) {
     lors_status_t st = check_problem(p);
     if (st != LORS_OK) return st;
-    const void* all[] = {dY, X, W, M_packed, B, A, dX, dB, dA, dbias};
+    const size_t need = lors_workspace_bytes(p);
+    const void* all[] = {dY, X, W, M_packed, B, A, dX, dB, dA, dbias, need ? workspace : nullptr};
     for (const void* q : all)
         if (q && !aligned16(q)) return LORS_ERR_ALIGN;
     const int64_t es = elt_size(p->dtype);
@@ -271,27 +278,37 @@ lors_status_t check_backward(const lors_problem_t* p, const void* dY, const void
                          range_of(M_packed, static_cast<int64_t>(lors_mask_packed_bytes(R, C))),
                          range_of(B, R * r * es), range_of(A, r * C * es)};
     const Range outs[] = {dX ? range_of(dX, L * C * es) : Range{0, 0}, dB ? range_of(dB, R * r * 4) : Range{0, 0},
-                          dA ? range_of(dA, r * C * 4) : Range{0, 0}, dbias ? range_of(dbias, R * 4) : Range{0, 0}};
-    for (int o = 0; o < 4; ++o) {
+                          dA ? range_of(dA, r * C * 4) : Range{0, 0}, dbias ? range_of(dbias, R * 4) : Range{0, 0},
+                          (need && workspace) ? range_of(workspace, static_cast<int64_t>(need)) : Range{0, 0}};
+    for (int o = 0; o < 5; ++o) {
         for (const Range& in : ins)
             if (overlap(outs[o], in)) return LORS_ERR_ALIAS;
-        for (int o2 = o + 1; o2 < 4; ++o2)
+        for (int o2 = o + 1; o2 < 5; ++o2)
             if (overlap(outs[o], outs[o2])) return LORS_ERR_ALIAS;
     }
-    if (workspace_bytes < lors_workspace_bytes(p)) return LORS_ERR_WORKSPACE;
+    if (need && (workspace == nullptr || workspace_bytes < need)) return LORS_ERR_WORKSPACE;
     return LORS_OK;
 }
 
 lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* X, const void* W,
                            const uint32_t* M_packed, const void* B, const void* A, void* dX, float* dB,
-                           float* dA, float* dbias) {
+                           float* dA, float* dbias, void* workspace) {
     lors::LayerArgs a{};
     a.R = p->R; a.C = p->C; a.L = p->L; a.r = p->r;
     a.scale = p->scale;
     a.two_four = p->mask_format == LORS_MASK_2_4;
     a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.dY = dY;
     a.dX = dX; a.dB = dB; a.dA = dA; a.dbias = dbias;
+    a.Mt = (p->dtype == LORS_DTYPE_BF16) ? static_cast<const uint32_t*>(workspace) : nullptr;
+    a.reuse_mt = (p->flags & LORS_FLAG_REUSE_MASK_T) != 0u;
     return a;
+}
+
+// M^T into the workspace (bf16 problems with tokens only, unless the caller
+// says the workspace already holds it).
+hipError_t build_mt(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
+    if (!bf16 || a.L == 0 || a.reuse_mt) return hipSuccess;
+    return lors::launch_mask_transpose(a.M, a.R, a.C, a.two_four, const_cast<uint32_t*>(a.Mt), s);
 }
 
 hipError_t run_weight(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
@@ -311,14 +328,13 @@ lors_status_t lors_backward(const lors_problem_t* p, const void* dY, const void*
     if ((tok && (dY == nullptr || X == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
         A == nullptr || dB == nullptr || dA == nullptr)
         return LORS_ERR_NULL;
-    lors_status_t st = check_backward(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace_bytes);
+    lors_status_t st = check_backward(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace, workspace_bytes);
     if (st != LORS_OK) return st;
-    (void)workspace;
-    const lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias);
+    const lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool bf16 = p->dtype == LORS_DTYPE_BF16;
-    hipError_t e = hipSuccess;
-    if (dX) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
+    hipError_t e = build_mt(a, bf16, s);
+    if (e == hipSuccess && dX) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
     if (e == hipSuccess) e = run_weight(a, bf16, s);
     return from_hip(e);
 }
@@ -331,13 +347,15 @@ lors_status_t lors_backward_data(const lors_problem_t* p, const void* dY, const 
     if ((tok && (dY == nullptr || dX == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
         A == nullptr)
         return LORS_ERR_NULL;
-    lors_status_t st = check_backward(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr,
+    lors_status_t st = check_backward(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr, workspace,
                                       workspace_bytes);
     if (st != LORS_OK) return st;
-    (void)workspace;
-    const lors::LayerArgs a = layer_args(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr);
+    const lors::LayerArgs a = layer_args(p, dY, nullptr, W, M_packed, B, A, dX, nullptr, nullptr, nullptr, workspace);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s));
+    const bool bf16 = p->dtype == LORS_DTYPE_BF16;
+    hipError_t e = build_mt(a, bf16, s);
+    if (e == hipSuccess) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
+    return from_hip(e);
 }
 
 lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY, const void* X, const uint32_t* M_packed,
@@ -348,11 +366,15 @@ lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY, cons
     if ((tok && (dY == nullptr || X == nullptr)) || M_packed == nullptr || B == nullptr || A == nullptr ||
         dB == nullptr || dA == nullptr)
         return LORS_ERR_NULL;
-    lors_status_t st = check_backward(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias, workspace_bytes);
+    lors_status_t st = check_backward(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias, workspace,
+                                      workspace_bytes);
     if (st != LORS_OK) return st;
-    (void)workspace;
-    const lors::LayerArgs a = layer_args(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias);
-    return from_hip(run_weight(a, p->dtype == LORS_DTYPE_BF16, static_cast<hipStream_t>(stream)));
+    const lors::LayerArgs a = layer_args(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias, workspace);
+    const bool bf16 = p->dtype == LORS_DTYPE_BF16;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = build_mt(a, bf16, s);
+    if (e == hipSuccess) e = run_weight(a, bf16, s);
+    return from_hip(e);
 }
 
 }  // extern "C"

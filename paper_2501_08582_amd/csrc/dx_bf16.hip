@@ -3,51 +3,61 @@
 //   dX[L x C] = dY[L x R] . W',   W' = select(M, W + s.B.A, 0)
 //
 // (dX step of the SP-LoRA backward list in Section 2.2; the merged weight is
-// recomputed instead of stored, Algorithm 2 / Section 2.3.)  The GEMM runs
-// over K = R.  Each K-step stages the dY tile and the raw W tile (64 rows of
-// R, natural layout), rebuilds W' for that tile with a rank-r MFMA, and writes
-// W' transposed into LDS so that both MFMA operands are read K-contiguous.
-#include "device_common.hpp"
+// recomputed instead of stored, Algorithm 2 / Section 2.3.)  GEMM over K = R.
+//
+// Same structure as the forward: each of the 4 waves owns 64 input features
+// (n) of the 256 x 256 tile and rebuilds W'[k][n] for its columns in
+// registers, in the B-operand layout of the main MFMA (rank-r MFMA with its
+// k rows taken in the order pi, see the forward kernel).  Differences:
+//   * W is stored [k][n] (k = R), so the raw W values a lane needs -- eight
+//     consecutive k of one column n -- come from two LDS transpose loads;
+//   * the k-rows of the rank-r product are B[k][:], read from a B slab copied
+//     contiguously into LDS each K-step; A[:, n] is resident in registers;
+//   * the mask bits a lane needs run along k for a fixed n, so they are read
+//     from the transposed bitmap M^T (built once per backward call).
+// Requires r % 8 == 0 and r <= 64 (other ranks use the LDS-merge kernel).
+#include "gemm_common.hpp"
 #include "kernels.hpp"
 
 namespace lors {
 namespace {
 
-constexpr int BM = 256;  // tokens per tile (GEMM M)
-constexpr int BN = 256;  // input features per tile (GEMM N)
-constexpr int BK = 64;   // rows of W (output features) per K-step
-constexpr int NT = 512;
-constexpr int WM = 2, WN = 4;
-constexpr int FM = BM / WM / 32;
-constexpr int FN = BN / WN / 32;
-constexpr int LDT = BK + 8;   // pitch of the dY tile and of the transposed W' tile
-constexpr int LDW = BN + 8;   // pitch of the raw W tile (rows of R)
+constexpr int NT = 256;
+constexpr int BM = 256;  // tokens per tile
+constexpr int BN = 256;  // input features per tile (64 per wave)
+constexpr int BK = 64;   // output features (rows of W) per K-step
 constexpr int GROUP_M = 4;
 
-static_assert(BN / 32 == NT / kWave, "one merge n-block per wave");
+constexpr int DB = BM * kRow64;      // dY slab: 32 KiB
+constexpr int WB = BK * kRowBytes;   // W slab [k][n]: 32 KiB
+constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 
-constexpr int kDsBytes = BM * LDT * 2;
-constexpr int kWnBytes = BK * LDW * 2;
-constexpr int kWtBytes = BN * LDT * 2;
-constexpr int kSmemBytes = kDsBytes + kWnBytes + kWtBytes;
+template <int RK>
+struct Layout {
+    static constexpr int BB = BK * 32 * RK;        // B slab [k][r], pitch 2r <= 32*RK bytes
+    static constexpr int D = 0, W = DB, B = DB + WB, M = DB + WB + BB;
+    static constexpr int STAGE = DB + WB + BB + MB;
+    static constexpr int LUT = 2 * STAGE;
+    static constexpr int DUMMY = LUT + 4096;
+    static constexpr int TOTAL = DUMMY + 1024;
+    static constexpr int NB = (2 * RK + 3) / 4;    // B-slab copies per wave (r/8 copies in all)
+    static constexpr int LOADS = 8 + 8 + NB + 2;
+};
 
-template <int RK, bool TWO_FOUR>
+template <int RK, bool TWO_FOUR_UNUSED>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
-    const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
-    const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C,
-    int r, float s, int tiles_m, int tiles_n) {
-    constexpr int LDA = RK * 16 + 8;  // pitch of the transposed A block (rows = n)
-    static_assert(BN * LDA * 2 <= kWnBytes + kWtBytes, "A block fits the W regions");
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kSmemBytes];
-    uint16_t* Ds = (uint16_t*)smem;                            // [m][k]
-    uint16_t* Wn = (uint16_t*)(smem + kDsBytes);               // [k][n] raw W
-    uint16_t* Wt = (uint16_t*)(smem + kDsBytes + kWnBytes);    // [n][k] W'
-    uint16_t* Ast = (uint16_t*)(smem + kDsBytes);              // [n][j], prologue only
+    const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
+    const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
+    float s, int tiles_m, int tiles_n) {
+    using Lay = Layout<RK>;
+    static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
+    static_assert(16 * RK * kRowBytes <= Lay::STAGE, "A block fits one stage");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
@@ -56,148 +66,163 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const int64_t m0 = (int64_t)tm * BM;
     const int n0 = tn * BN;
     const int nk = (R + BK - 1) / BK;
-    const int wpr = (C + 31) >> 5;
-    const bool b_vec = (r & 7) == 0;
+    const int wprT = (R + 31) >> 5;  // words per row of M^T
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+    const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
+    const int slab_b = 2 * r;        // bytes per B row
+    const int nbcopies = r >> 3;     // 1 KiB copies per B slab (64 rows x 2r bytes)
 
-    // Prologue: A[:, n0 .. n0+255] transposed into LDS, then each wave keeps
-    // the merge operand A^T[32*wave + l32][16c + 8h .. +7] in registers.
-    for (int c = tid; c < RK * 16 * (BN / 8); c += NT) {
-        const int j = c / (BN / 8), nc = c % (BN / 8);
-        const int gn = n0 + nc * 8;
-        const u32x4 v = (j < r && gn < C) ? *(const u32x4*)(Am + (int64_t)j * C + gn) : zero_u32x4();
+    // M^T is a plain bitmap whatever the caller's layout.
+    *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
+
+    // ---- prologue: A[:, n0 .. n0+255] (16*RK rows) -> stage 1, then the
+    // merge's B operand A[16c + 8h + e][n] into registers via transpose loads.
 #pragma unroll
-        for (int e = 0; e < 8; ++e) Ast[(nc * 8 + e) * LDA + j] = (uint16_t)u16_at(v, e);
+    for (int q = 0; q < 2 * RK; ++q) {
+        const int blk = 4 * q + wave;
+        const int row = 2 * blk + h;
+        const int lc = swz_chunk(row, lane & 31);
+        const int gn = n0 + 8 * lc;
+        copy16_to_lds((row < r && gn < C) ? (const void*)(Am + (int64_t)row * C + gn) : (const void*)zsrc,
+                      lds0 + Lay::STAGE + 1024 * blk);
     }
-    __syncthreads();
-    bf16x8 afr[RK];
+    stage_barrier<0>();
+    bf16x8 afr[2][RK];
 #pragma unroll
-    for (int c = 0; c < RK; ++c)
-        afr[c] = *(const bf16x8*)(Ast + (wave * 32 + l32) * LDA + 16 * c + 8 * h);
-    __syncthreads();
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int c = 0; c < RK; ++c)
+            afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 0)),
+                                      lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
+    lds_barrier();
 
-    const int nw = (n0 >> 5) + wave;  // mask word column of this wave's merge rows
-    u32x4 dr[4], wr[4];
-    bf16x8 bfr[2][RK];
-    uint32_t mw[2];
-
-    auto load_tiles = [&](int kt) {
+    auto issue = [&](int kt, int st) {
         const int k0 = kt * BK;
+        const uint32_t sb = lds0 + st * Lay::STAGE;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int c = tid + q * NT;
-            {   // dY tile: 256 rows (tokens) x 64 columns (R)
-                const int row = c >> 3, kc = c & 7;
-                const int gk = k0 + kc * 8;
+        for (int q = 0; q < 8; ++q) {
+            const int blk = 8 * wave + q;
+            {   // dY slab: rows m, 64 k per row
+                const int row = 8 * blk + (lane >> 3);
+                const int lc = (lane & 7) ^ ((row >> 1) & 7);
+                const int gk = k0 + 8 * lc;
                 const int64_t gm = m0 + row;
-                dr[q] = (gm < L && gk < R) ? *(const u32x4*)(dY + gm * R + gk) : zero_u32x4();
+                copy16_to_lds((gm < L && gk < R) ? (const void*)(dY + gm * R + gk) : (const void*)zsrc,
+                              sb + Lay::D + 1024 * blk);
             }
-            {   // raw W tile: 64 rows (R) x 256 columns (C)
-                const int row = c >> 5, nc = c & 31;
-                const int gk = k0 + row, gn = n0 + nc * 8;
-                wr[q] = (gk < R && gn < C) ? *(const u32x4*)(W + (int64_t)gk * C + gn) : zero_u32x4();
+            {   // W slab: rows k, 256 n per row
+                const int row = 2 * blk + h;
+                const int lc = swz_chunk(row, lane & 31);
+                const int gk = k0 + row, gn = n0 + 8 * lc;
+                copy16_to_lds((gk < R && gn < C) ? (const void*)(W + (int64_t)gk * C + gn) : (const void*)zsrc,
+                              sb + Lay::W + 1024 * blk);
             }
         }
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int gk = k0 + 32 * kb + l32;
+        for (int q = 0; q < Lay::NB; ++q) {  // B rows k0 .. k0+63: one contiguous block
+            const int blk = 4 * q + wave;
+            const bool real = blk < nbcopies;
+            const int off = 1024 * blk + 16 * lane;   // byte offset inside the slab
+            const bool ok = real && k0 + off / slab_b < R;
+            copy16_to_lds(ok ? (const void*)((const uint8_t*)Bm + (int64_t)k0 * slab_b + off) : (const void*)zsrc,
+                          real ? sb + Lay::B + 1024 * blk : lds0 + Lay::DUMMY);
+        }
 #pragma unroll
-            for (int c = 0; c < RK; ++c) {
-                u32x4 v = zero_u32x4();
-                if (gk < R) {
-                    const uint16_t* src = Bm + (int64_t)gk * r + 16 * c + 8 * h;
-                    if (b_vec) {
-                        if (16 * c + 8 * h < r) v = *(const u32x4*)src;
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const uint32_t x = (16 * c + 8 * h + e < r) ? (uint32_t)src[e] : 0u;
-                            v[e >> 1] |= x << ((e & 1) * 16);
-                        }
-                    }
-                }
-                bfr[kb][c] = as_bf16x8(v);
-            }
-            mw[kb] = (gk < R && nw < wpr) ? Mp[(int64_t)gk * wpr + nw] : 0u;
+        for (int q = 0; q < 2; ++q) {      // M^T words: [n][kb]
+            const int e = 64 * (2 * wave + q) + lane;
+            const int n = e >> 1, kb = e & 1;
+            const int gw = (k0 >> 5) + kb;
+            const int gn = n0 + n;
+            copy4_to_lds((gn < C && gw < wprT) ? (const void*)(Mt + (int64_t)gn * wprT + gw) : (const void*)zsrc,
+                         sb + Lay::M + 256 * (2 * wave + q));
         }
     };
 
-    f32x16 acc[FM][FN];
+    // Rows of the merge A operand: lane (rho = l32, h) reads B row pi(rho).
+    const int rho = l32;
+    const int pik = 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho >> 3) & 1) + (rho & 3);
+    const int ncol[2] = {64 * wave + l32, 64 * wave + 32 + l32};
+
+    f32x16 acc[8][2];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int wm = wave / WN, wn = wave % WN;
+    issue(0, 0);
+    if (nk > 1) issue(1, 1);
 
-    load_tiles(0);
     for (int kt = 0; kt < nk; ++kt) {
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int c = tid + q * NT;
-            *(u32x4*)(Ds + (c >> 3) * LDT + (c & 7) * 8) = dr[q];
-            *(u32x4*)(Wn + (c >> 5) * LDW + (c & 31) * 8) = wr[q];
-        }
-        __syncthreads();
+        const int st = kt & 1;
+        if (kt + 1 < nk)
+            stage_barrier<Lay::LOADS>();
+        else
+            stage_barrier<0>();
+        const uint8_t* sb = smem + st * Lay::STAGE;
 
-        // Merge: C[n][k] = sum_j A[j][n] B[k][j] for this wave's 32 columns n
-        // and the 64 rows k of the step; lane (l32, h) owns row k = 32kb + l32
-        // and columns n = 32*wave + 8i + 4h + q.
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            f32x16 T;
+            bf16x8 bfr[RK];  // B[32kb + pi(rho)][16c + 8h .. +7]
 #pragma unroll
-            for (int v = 0; v < 16; ++v) T[v] = 0.f;
+            for (int c = 0; c < RK; ++c) {
+                const int j0 = 16 * c + 8 * h;
+                u32x4 v = zero_u32x4();
+                if (j0 < r) v = *(const u32x4*)(sb + Lay::B + (32 * kb + pik) * slab_b + 2 * j0);
+                bfr[c] = as_bf16x8(v);
+            }
+            bf16x8 wf[2][2];
 #pragma unroll
-            for (int c = 0; c < RK; ++c) T = mfma_32x32x16(afr[c], bfr[kb][c], T);
-            const int kl = 32 * kb + l32;
+            for (int nb = 0; nb < 2; ++nb) {
+                f32x16 T;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int nl = wave * 32 + 8 * i + 4 * h;
-                const u32x2 wv = *(const u32x2*)(Wn + kl * LDW + nl);
-                const uint32_t keep = keep4<TWO_FOUR>(mw[kb], 8 * i + 4 * h);
-                float w0 = fmaf(s, T[4 * i + 0], bf16_bits_to_f32(wv[0] & 0xFFFFu));
-                float w1 = fmaf(s, T[4 * i + 1], bf16_bits_to_f32(wv[0] >> 16));
-                float w2 = fmaf(s, T[4 * i + 2], bf16_bits_to_f32(wv[1] & 0xFFFFu));
-                float w3 = fmaf(s, T[4 * i + 3], bf16_bits_to_f32(wv[1] >> 16));
-                Wt[(nl + 0) * LDT + kl] = (keep & 1u) ? bf16_bits(w0) : (uint16_t)0;
-                Wt[(nl + 1) * LDT + kl] = (keep & 2u) ? bf16_bits(w1) : (uint16_t)0;
-                Wt[(nl + 2) * LDT + kl] = (keep & 4u) ? bf16_bits(w2) : (uint16_t)0;
-                Wt[(nl + 3) * LDT + kl] = (keep & 8u) ? bf16_bits(w3) : (uint16_t)0;
+                for (int v = 0; v < 16; ++v) T[v] = 0.f;
+#pragma unroll
+                for (int c = 0; c < RK; ++c) T = mfma_32x32x16(bfr[c], afr[nb][c], T);
+                const uint32_t word = *(const uint32_t*)(sb + Lay::M + 8 * ncol[nb] + 4 * kb);
+#pragma unroll
+                for (int cp = 0; cp < 2; ++cp) {
+                    const int row0 = 32 * kb + 16 * cp;
+                    const u32x2 lo = lds_tr_read(sb + Lay::W + tr_frag_off(lane, row0, 64 * wave + 32 * nb, 0));
+                    const u32x2 hi = lds_tr_read(sb + Lay::W + tr_frag_off(lane, row0, 64 * wave + 32 * nb, 1));
+                    u32x4 raw;
+                    raw[0] = lo[0]; raw[1] = lo[1]; raw[2] = hi[0]; raw[3] = hi[1];
+                    const uint32_t byte = (word >> (8 * (2 * cp + h))) & 0xFFu;
+                    const u32x4 sel = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+                    float t8[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) t8[e] = T[8 * cp + e];
+                    wf[nb][cp] = as_bf16x8(merge8(raw, t8, s, sel));
+                }
+            }
+#pragma unroll
+            for (int cp = 0; cp < 2; ++cp) {
+                const int c4 = 2 * kb + cp;
+                bf16x8 df[8];
+#pragma unroll
+                for (int mb = 0; mb < 8; ++mb)
+                    df[mb] = *(const bf16x8*)(sb + Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h));
+#pragma unroll
+                for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+                    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(df[mb], wf[nb][cp], acc[mb][nb]);
             }
         }
-        __syncthreads();
-
-        if (kt + 1 < nk) load_tiles(kt + 1);
-
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8 a[FM], b[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-                a[i] = *(const bf16x8*)(Ds + (wm * (BM / WM) + 32 * i + l32) * LDT + 16 * ks + 8 * h);
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-                b[j] = *(const bf16x8*)(Wt + (wn * (BN / WN) + 32 * j + l32) * LDT + 16 * ks + 8 * h);
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(a[i], b[j], acc[i][j]);
-        }
+        lds_barrier();
+        if (kt + 2 < nk) issue(kt + 2, st);
     }
 
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int gn = n0 + wn * (BN / WN) + 32 * j + l32;
+    for (int nb = 0; nb < 2; ++nb) {
+        const int gn = n0 + ncol[nb];
         if (gn >= C) continue;
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
+        for (int mb = 0; mb < 8; ++mb) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int64_t gm = m0 + wm * (BM / WM) + 32 * i + 8 * (v >> 2) + 4 * h + (v & 3);
-                if (gm < L) dX[gm * C + gn] = bf16_bits(acc[i][j][v]);
+                const int64_t gm = m0 + 32 * mb + 8 * (v >> 2) + 4 * h + (v & 3);
+                if (gm < L) dX[gm * C + gn] = bf16_bits(acc[mb][nb][v]);
             }
         }
     }
@@ -208,17 +233,9 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
-    auto* dY = (const uint16_t*)a.dY;
-    auto* W = (const uint16_t*)a.W;
-    auto* B = (const uint16_t*)a.B;
-    auto* A = (const uint16_t*)a.A;
-    auto* dX = (uint16_t*)a.dX;
-    if (a.two_four)
-        hipLaunchKernelGGL((dx_kernel<RK, true>), grid, block, 0, st, dY, W, a.M, B, A, dX, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
-    else
-        hipLaunchKernelGGL((dx_kernel<RK, false>), grid, block, 0, st, dY, W, a.M, B, A, dX, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    hipLaunchKernelGGL((dx_kernel<RK, false>), grid, block, 0, st, (const uint16_t*)a.dY, (const uint16_t*)a.W,
+                       a.Mt, (const uint16_t*)a.B, (const uint16_t*)a.A, (uint16_t*)a.dX, a.L, (int)a.R,
+                       (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
 }
 
@@ -226,16 +243,13 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
 
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0 || a.dX == nullptr) return hipSuccess;
+    if (a.r % 8 != 0 || a.Mt == nullptr) return launch_dx_bf16_wide(a, st);
     switch ((a.r + 15) / 16) {
         case 1: return launch_rk<1>(a, st);
         case 2: return launch_rk<2>(a, st);
         case 3: return launch_rk<3>(a, st);
         case 4: return launch_rk<4>(a, st);
-        case 5: return launch_rk<5>(a, st);
-        case 6: return launch_rk<6>(a, st);
-        case 7: return launch_rk<7>(a, st);
-        case 8: return launch_rk<8>(a, st);
-        default: return hipErrorInvalidValue;
+        default: return launch_dx_bf16_wide(a, st);
     }
 }
 

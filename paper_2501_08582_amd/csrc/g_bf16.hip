@@ -11,7 +11,8 @@
 // shuffles data.  Four waves each own a 128 x 128 block of the 256 x 256 G
 // tile (fp32 accumulators in AGPRs); LDS is double-buffered.
 //
-// Epilogue: the accumulators are masked in registers and rounded to bf16.
+// Epilogue: the accumulators are masked in registers (keep bits from the
+// transposed bitmap M^T, one word per lane and 32 rows) and rounded to bf16.
 // dA uses them directly as the MFMA B operand (contraction over the rows of G
 // in the accumulator's own row order); dB reads G^T back from LDS.  Per-tile
 // partial sums are added into dB and dA with fp32 atomics, so dB and dA must
@@ -32,22 +33,25 @@ constexpr int SMEM = 2 * STAGEB;       // two stages
 constexpr int GROUP_M = 4;
 constexpr int LOADS = TILEB / 1024 / (NT / kWave);  // 1 KiB copies per wave per slab (8)
 
-// Epilogue LDS carve-up (reuses the stage buffers).
+// Epilogue LDS carve-up (reuses the stage buffers; EP_A lies past them).
 constexpr int GT_PITCH = 512;                      // G^T tile: [j][i], 256 i per row
 constexpr int GT_BYTES = BN * GT_PITCH;            // 128 KiB
-constexpr int MASK_OFF = 0;                        // mask tile [i][8 words] (before G^T)
-constexpr int BT_PITCH = BM + 8;                   // B^T tile [j'][i], elements per row
+constexpr int EP_MT = 0;                           // M^T words [j][8]: 8 KiB
+constexpr int EP_LUT = 8192;                       // select LUT: 4 KiB
+constexpr int EP_B = 12288;                        // B block [i][32*JB] bf16: up to 64 KiB
+constexpr int EP_A = SMEM;                         // A block [32 j'][256 j]: 16 KiB
+constexpr int SMEM_ALL = SMEM + 32 * kRowBytes;
 
-template <int RK, bool TWO_FOUR>
+template <int RK>
 __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
-    const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
+    const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, float* __restrict__ dB, float* __restrict__ dA,
     int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n) {
     constexpr int JB = (RK + 1) / 2;  // 32-wide blocks of the rank
     static_assert(GT_BYTES <= SMEM, "G^T tile fits");
-    static_assert(JB * 32 * BT_PITCH * 2 <= SMEM, "B^T tile fits");
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
+    static_assert(EP_B + BM * 32 * JB * 2 <= SMEM, "B block fits");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM_ALL];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -61,7 +65,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const int i0 = tm * BM;
     const int j0 = tn * BN;
     const int64_t nk = (L + BK - 1) / BK;
-    const int wpr = (C + 31) >> 5;
+    const int wprT = (R + 31) >> 5;  // words per row of M^T
 
     // ---- asynchronous slab copies: copy q of this wave fills tile rows
     // 2*(8*wave + q) + {0, 1}; lane l covers physical chunk l % 32 of its row.
@@ -129,45 +133,85 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     }
     stage_barrier<0>();
 
-    // ---- epilogue 1: mask words of the tile -> LDS as [i][8 words].
-    uint32_t* msk = (uint32_t*)(smem + MASK_OFF);
-    for (int e = tid; e < BM * 8; e += NT) {
-        const int il = e >> 3, w = e & 7;
-        const int gi = i0 + il, gw = (j0 >> 5) + w;
-        msk[e] = (gi < R && gw < wpr) ? Mp[(int64_t)gi * wpr + gw] : 0u;
+    // ---- epilogue 1: side data into the (now idle) stage buffers:
+    //   M^T words of the tile [j][8 words], the select LUT, and B[i0.., :]
+    //   as [i][32*JB] (rank padded with zeros).
+    uint32_t* mtl = (uint32_t*)(smem + EP_MT);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int blk = 8 * wave + q;          // 32 copies of 64 words
+        const int e = 64 * blk + lane;
+        const int j = e >> 3, iw = e & 7;
+        const int gj = j0 + j, giw = (i0 >> 5) + iw;
+        copy4_to_lds((gj < C && giw < wprT) ? (const void*)(Mt + (int64_t)gj * wprT + giw) : (const void*)zsrc,
+                     lds0 + EP_MT + 256 * blk);
     }
-    __syncthreads();
+    *(u32x4*)(smem + EP_LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
+    uint16_t* btl = (uint16_t*)(smem + EP_B);
+    for (int e = tid; e < BM * 32 * JB; e += NT) {
+        const int il = e / (32 * JB), jr = e % (32 * JB);
+        const int gi = i0 + il;
+        btl[e] = (gi < R && jr < r) ? Bm[(int64_t)gi * r + jr] : (uint16_t)0;
+    }
+    stage_barrier<0>();
 
-    // ---- epilogue 2: select by the mask, round to bf16, keep the packed
-    // fragments: gb[a][b][c] holds accumulator elements 8c .. 8c+7 of block
-    // (a, b) (rows 16c + 4h + {0..3} and 16c + 8 + 4h + {0..3}).
+    // ---- epilogue 2: select by the mask, round to bf16.  gb[a][b][c] holds
+    // accumulator elements 8c .. 8c+7 of block (a, b): rows 16c + 4h + {0..3}
+    // and 16c + 8 + 4h + {0..3} of column j = l32.
     u32x4 gb[4][4][2];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
+        for (int b = 0; b < 4; ++b) {
+            const int jl = wj * 128 + 32 * b + l32;
+            const uint32_t word = mtl[jl * 8 + wi * 4 + a];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int il = wi * 128 + 32 * a + 8 * v4 + 4 * h + q;
-                const u32x4 words = *(const u32x4*)(msk + il * 8 + wj * 4);
+            for (int c = 0; c < 2; ++c) {
+                const uint32_t byte = ((word >> (16 * c + 4 * h)) & 0xFu) | (((word >> (16 * c + 8 + 4 * h)) & 0xFu) << 4);
+                const u32x4 sel = *(const u32x4*)(smem + EP_LUT + 16 * byte);
 #pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const uint32_t keep = keep1<TWO_FOUR>(words[b], (uint32_t)l32);
-                    acc[a][b][4 * v4 + q] = keep ? acc[a][b][4 * v4 + q] : 0.f;
+                for (int p = 0; p < 4; ++p)
+                    gb[a][b][c][p] = pack_bf16x2(acc[a][b][8 * c + 2 * p], acc[a][b][8 * c + 2 * p + 1]) & sel[p];
+            }
+        }
+
+    // ---- epilogue 3: dA[j'][j] += s * sum_i B[i][j'] G[i][j], with the masked
+    // bf16 accumulators as the MFMA B operand (K = rows i in accumulator
+    // order); the A operand B^T comes from the B block by transpose loads.
+    {
+        const int g = lane >> 4, jj = lane & 15;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int gj = j0 + wj * 128 + 32 * b + l32;
+#pragma unroll
+            for (int jb = 0; jb < JB; ++jb) {
+                f32x16 da;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) da[v] = 0.f;
+                const int col = 32 * jb + 16 * (g & 1) + 4 * (jj & 3);
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) {
+                        const int row = wi * 128 + 32 * a + 16 * c + 4 * (g >> 1) + (jj >> 2);
+                        const u32x2 lo = lds_tr_read(smem + EP_B + 2 * (row * 32 * JB + col));
+                        const u32x2 hi = lds_tr_read(smem + EP_B + 2 * ((row + 8) * 32 * JB + col));
+                        da = mfma_32x32x16(frag_from_tr(lo, hi), as_bf16x8(gb[a][b][c]), da);
+                    }
+                }
+                if (gj < C) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
+                        if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
+                    }
                 }
             }
         }
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    gb[a][b][c][e] = pack_bf16x2(acc[a][b][8 * c + 2 * e], acc[a][b][8 * c + 2 * e + 1]);
     }
-    __syncthreads();  // mask tile no longer needed
+    lds_barrier();
 
-    // ---- epilogue 3: G^T -> LDS as [j][i] (pitch 512 B; the quad of 16-byte
+    // ---- epilogue 4: G^T -> LDS as [j][i] (pitch 512 B; the quad of 16-byte
     // chunks is XORed with j % 8 so that transpose reads of 4 consecutive j
     // hit different banks).  Lane (j, h) stores rows 8*v4 + 4h + {0..3}.
     auto gt_off = [](int j, int i) {
@@ -181,96 +225,53 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4) {
                 const int il = wi * 128 + 32 * a + 8 * v4 + 4 * h;
-                const u32x4& g = gb[a][b][v4 >> 1];
+                const u32x4& gv = gb[a][b][v4 >> 1];
                 u32x2 o;
-                o[0] = g[2 * (v4 & 1)];
-                o[1] = g[2 * (v4 & 1) + 1];
+                o[0] = gv[2 * (v4 & 1)];
+                o[1] = gv[2 * (v4 & 1) + 1];
                 *(u32x2*)(smem + gt_off(jl, il)) = o;
             }
         }
-    __syncthreads();
 
-    // ---- epilogue 4: dB[i][j'] += s * sum_j G[i][j] A[j'][j].  Wave w owns
-    // tile rows 64w .. 64w+63.  A operand (rows i, 8 consecutive j) is read
-    // from G^T with the transpose load; B operand straight from A in HBM.
+    // ---- epilogue 5: dB[i][j'] += s * sum_j G[i][j] A[j'][j], one 32-wide
+    // rank block at a time: A[32jb .. +31][j0 .. j0+255] is copied to LDS and
+    // wave w accumulates rows i = 64w .. 64w+63 of the tile.
+    for (int jb = 0; jb < JB; ++jb) {
 #pragma unroll
-    for (int ib = 0; ib < 2; ++ib) {
-        const int irow0 = 64 * wave + 32 * ib;
-        f32x16 db[JB];
+        for (int q = 0; q < 4; ++q) {          // 32 rows x 512 B = 16 copies, 4 per wave
+            const int blk = 4 * wave + q;
+            const int row = 2 * blk + h;
+            const int lc = swz_chunk(row, lane & 31);
+            const int jr = 32 * jb + row, gj = j0 + 8 * lc;
+            copy16_to_lds((jr < r && gj < C) ? (const void*)(Am + (int64_t)jr * C + gj) : (const void*)zsrc,
+                          lds0 + EP_A + 1024 * blk);
+        }
+        stage_barrier<0>();  // A block landed; G^T complete
 #pragma unroll
-        for (int b = 0; b < JB; ++b)
+        for (int ib = 0; ib < 2; ++ib) {
+            const int irow0 = 64 * wave + 32 * ib;
+            f32x16 db;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) db[b][v] = 0.f;
-        for (int kc = 0; kc < BN / 16; ++kc) {
-            // transpose read from the [j][i] tile: rows j, columns i
-            u32x2 lo, hi;
-            {
-                const int g = lane >> 4, jj = lane & 15;
+            for (int v = 0; v < 16; ++v) db[v] = 0.f;
+            const int g = lane >> 4, jj = lane & 15;
+#pragma unroll 4
+            for (int kc = 0; kc < BN / 16; ++kc) {
                 const int jr0 = 16 * kc + 8 * (g >> 1) + (jj >> 2);
                 const int ic = irow0 + 16 * (g & 1) + 4 * (jj & 3);
-                lo = lds_tr_read(smem + gt_off(jr0, ic));
-                hi = lds_tr_read(smem + gt_off(jr0 + 4, ic));
+                const bf16x8 ga = frag_from_tr(lds_tr_read(smem + gt_off(jr0, ic)), lds_tr_read(smem + gt_off(jr0 + 4, ic)));
+                const bf16x8 av = *(const bf16x8*)(smem + EP_A + tile_off(l32, 16 * kc + 8 * h));
+                db = mfma_32x32x16(ga, av, db);
             }
-            const bf16x8 ga = frag_from_tr(lo, hi);
-            const int gj = j0 + 16 * kc + 8 * h;
-#pragma unroll
-            for (int b = 0; b < JB; ++b) {
-                const int jr = 32 * b + l32;
-                const u32x4 av = (jr < r && gj < C) ? *(const u32x4*)(Am + (int64_t)jr * C + gj) : zero_u32x4();
-                db[b] = mfma_32x32x16(ga, as_bf16x8(av), db[b]);
-            }
-        }
-#pragma unroll
-        for (int b = 0; b < JB; ++b) {
-            const int jr = 32 * b + l32;
-            if (jr >= r) continue;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int gi = i0 + irow0 + 8 * (v >> 2) + 4 * h + (v & 3);
-                if (gi < R) atomicAdd(dB + (int64_t)gi * r + jr, s * db[b][v]);
-            }
-        }
-    }
-    __syncthreads();
-
-    // ---- epilogue 5: B^T of the tile's rows -> LDS as [j'][i] (padded pitch).
-    uint16_t* bt = (uint16_t*)smem;
-    for (int e = tid; e < BM * JB * 32; e += NT) {
-        const int il = e / (JB * 32), jr = e % (JB * 32);
-        const int gi = i0 + il;
-        bt[jr * BT_PITCH + il] = (gi < R && jr < r) ? Bm[(int64_t)gi * r + jr] : (uint16_t)0;
-    }
-    __syncthreads();
-
-    // ---- epilogue 6: dA[j'][j] += s * sum_i B[i][j'] G[i][j] with the masked
-    // bf16 accumulators as the B operand (K = rows i in accumulator order).
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        const int gj = j0 + wj * 128 + 32 * b + l32;
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) {
-            f32x16 da;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) da[v] = 0.f;
-#pragma unroll
-            for (int a = 0; a < 4; ++a) {
-                const int ib = wi * 128 + 32 * a;
-#pragma unroll
-                for (int c = 0; c < 2; ++c) {
-                    const uint16_t* p = bt + (32 * jb + l32) * BT_PITCH + ib + 16 * c + 4 * h;
-                    const u32x2 lo = *(const u32x2*)p;
-                    const u32x2 hi = *(const u32x2*)(p + 8);
-                    da = mfma_32x32x16(frag_from_tr(lo, hi), as_bf16x8(gb[a][b][c]), da);
-                }
-            }
-            if (gj < C) {
+            const int jr = 32 * jb + l32;
+            if (jr < r) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
-                    if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
+                    const int gi = i0 + irow0 + 8 * (v >> 2) + 4 * h + (v & 3);
+                    if (gi < R) atomicAdd(dB + (int64_t)gi * r + jr, s * db[v]);
                 }
             }
         }
+        lds_barrier();  // A block free for the next rank block
     }
 }
 
@@ -283,12 +284,8 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     auto* X = (const uint16_t*)a.X;
     auto* B = (const uint16_t*)a.B;
     auto* A = (const uint16_t*)a.A;
-    if (a.two_four)
-        hipLaunchKernelGGL((g_kernel<RK, true>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
-    else
-        hipLaunchKernelGGL((g_kernel<RK, false>), grid, block, 0, st, dY, X, a.M, B, A, a.dB, a.dA, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    hipLaunchKernelGGL((g_kernel<RK>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
+                       (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
 }
 

@@ -51,6 +51,63 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_wave
 }
 #pragma clang diagnostic pop
 
+// ---------------------------------------------------------------------------
+// Slabs with 64 bf16 (128 bytes) per row, read one 16-byte chunk per lane
+// (ds_read_b128).  Chunk c of row `row` is stored at c ^ ((row >> 1) & 7):
+// the 16 lanes of one read pass (16 consecutive rows, same logical chunk)
+// then cover all 64 banks.
+// ---------------------------------------------------------------------------
+constexpr int kRow64 = 128;
+
+__device__ __forceinline__ int slab64_off(int row, int chunk) {
+    return row * kRow64 + ((chunk ^ ((row >> 1) & 7)) << 4);
+}
+
+// Element (row, col) of a 64-column slab.
+__device__ __forceinline__ int slab64_elem_off(int row, int col) {
+    return slab64_off(row, col >> 3) + ((col & 7) << 1);
+}
+
+// Byte-to-select LUT: entry b holds four 32-bit AND masks, one per packed
+// bf16 pair (2p, 2p+1), keeping element q iff bit q of the 8 keep bits is set.
+// For the 2:4 layout the byte is two group codes and the keep bits are
+// decoded from them.
+template <bool TWO_FOUR>
+__device__ __forceinline__ u32x4 select_lut_entry(uint32_t b) {
+    uint32_t keep = b;
+    if constexpr (TWO_FOUR) {
+        const uint32_t lo = b & 0xFu, hi = b >> 4;
+        keep = ((1u << (lo & 3u)) | (1u << (lo >> 2))) | (((1u << (hi & 3u)) | (1u << (hi >> 2))) << 4);
+    }
+    u32x4 e;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+        e[p] = (((keep >> (2 * p)) & 1u) ? 0x0000FFFFu : 0u) | (((keep >> (2 * p + 1)) & 1u) ? 0xFFFF0000u : 0u);
+    return e;
+}
+
+// W' = select(M, W + s.T, 0) for eight consecutive elements: raw holds the
+// eight bf16 of W (pairs), t the eight fp32 rank-r sums, sel the LUT masks.
+__device__ __forceinline__ u32x4 merge8(u32x4 raw, const float* t, float s, u32x4 sel) {
+    u32x4 out;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const float lo = __uint_as_float(raw[p] << 16);
+        const float hi = __uint_as_float(raw[p] & 0xFFFF0000u);
+        out[p] = pack_bf16x2(fmaf(s, t[2 * p], lo), fmaf(s, t[2 * p + 1], hi)) & sel[p];
+    }
+    return out;
+}
+
+// One 4-byte global -> LDS copy per lane (global_load_lds_dword): lane l's
+// word lands at lds_wave_base + 4*l.
+__device__ __forceinline__ void copy4_to_lds(const void* src, uint32_t lds_wave_base) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :
+                 : "v"(src), "s"(lds_wave_base)
+                 : "memory", "m0");
+}
+
 // Wait until at most N of this wave's vector-memory loads (including the
 // LDS copies above) are outstanding, then barrier: afterwards every copy
 // issued before the last N of every wave is visible in LDS.

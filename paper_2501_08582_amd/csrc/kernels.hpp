@@ -13,7 +13,9 @@ struct LayerArgs {
     bool two_four;          // packed mask layout: 2:4 codes (else bitmap)
     const void* X;          // L x C
     const void* W;          // R x C
-    const uint32_t* M;      // R x ceil(C/32)
+    const uint32_t* M;      // R x ceil(C/32), the caller's layout
+    const uint32_t* Mt;     // C x ceil(R/32) transposed bitmap (backward only)
+    bool reuse_mt;          // Mt already holds the transposed mask
     const void* B;          // R x r
     const void* A;          // r x C
     const void* bias;       // R or nullptr
@@ -27,7 +29,9 @@ struct LayerArgs {
 
 // bf16 path
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_fwd_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_dx_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_dbias_bf16(const LayerArgs& a, hipStream_t s);
 
@@ -46,6 +50,10 @@ hipError_t launch_mask_pack(const uint8_t* dense, int64_t R, int64_t C, bool two
 hipError_t launch_mask_from_weight(const void* W, bool w_is_bf16, int64_t R, int64_t C,
                                    bool two_four, uint32_t* packed, int64_t* first_bad,
                                    hipStream_t s);
+// Transposed bitmap of a packed mask: word j*ceil(R/32) + i/32, bit i % 32
+// is the keep bit of element (i, j).
+hipError_t launch_mask_transpose(const uint32_t* packed, int64_t R, int64_t C, bool two_four,
+                                 uint32_t* mt, hipStream_t s);
 hipError_t launch_mask_unpack(const uint32_t* packed, int64_t R, int64_t C, bool two_four,
                               uint8_t* dense, hipStream_t s);
 

@@ -118,6 +118,43 @@ __global__ __launch_bounds__(NT) void unpack_kernel(const uint32_t* __restrict__
     for (int e = 0; e < 32 && c0 + e < C; ++e) row[c0 + e] = (uint8_t)keep1<TWO_FOUR>(word, (uint32_t)e);
 }
 
+// Transposed bitmap: one wave handles a 32-row block of the mask and two
+// 32-column words.  Lane l < 32 reads row 32*iw + l of word jw, lane l >= 32
+// the same row of word jw + 1 (2:4 codes are first expanded to keep bits);
+// one ballot per bit position then yields, for every column, its 32 keep bits.
+template <bool TWO_FOUR>
+__global__ __launch_bounds__(NT) void transpose_kernel(const uint32_t* __restrict__ in, int64_t R, int C, int wpr,
+                                                       int wprT, uint32_t* __restrict__ out) {
+    const int lane = threadIdx.x & 63;
+    const int64_t task = (int64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+    const int jpairs = (wpr + 1) >> 1;
+    const int64_t iw = task / jpairs;
+    const int jw = (int)(task % jpairs) * 2 + (lane >> 5);
+    if (iw >= wprT) return;  // whole wave leaves together
+    const int64_t row = iw * 32 + (lane & 31);
+    uint32_t w = (row < R && jw < wpr) ? in[row * wpr + jw] : 0u;
+    if constexpr (TWO_FOUR) {
+        uint32_t keep = 0;
+#pragma unroll
+        for (int n = 0; n < 8; ++n) {
+            const uint32_t code = (w >> (4 * n)) & 0xFu;
+            keep |= ((1u << (code & 3u)) | (1u << (code >> 2))) << (4 * n);
+        }
+        // groups past C/4 hold no codes: clear their expansion
+        const int cols = C - 32 * jw;
+        w = cols >= 32 ? keep : (cols > 0 ? keep & ((1u << cols) - 1u) : 0u);
+    }
+    uint32_t mine = 0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) {
+        const uint64_t bal = __ballot((w >> b) & 1u);
+        const uint32_t lo = (uint32_t)bal, hi = (uint32_t)(bal >> 32);
+        mine = ((lane & 31) == b) ? (lane < 32 ? lo : hi) : mine;
+    }
+    const int64_t col = (int64_t)32 * jw + (lane & 31);
+    if (jw < wpr && col < C) out[col * wprT + iw] = mine;
+}
+
 __global__ __launch_bounds__(NT) void zero_kernel(float* __restrict__ p, int64_t n) {
     for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < n; t += (int64_t)gridDim.x * NT) p[t] = 0.f;
 }
@@ -197,6 +234,20 @@ hipError_t launch_mask_unpack(const uint32_t* packed, int64_t R, int64_t C, bool
         hipLaunchKernelGGL(unpack_kernel<true>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, dense);
     else
         hipLaunchKernelGGL(unpack_kernel<false>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, dense);
+    return hipGetLastError();
+}
+
+hipError_t launch_mask_transpose(const uint32_t* packed, int64_t R, int64_t C, bool two_four, uint32_t* mt,
+                                 hipStream_t st) {
+    const int wpr = (int)((C + 31) / 32);
+    const int wprT = (int)((R + 31) / 32);
+    const int64_t tasks = (int64_t)wprT * ((wpr + 1) / 2);
+    if (tasks == 0) return hipSuccess;
+    const unsigned blocks = (unsigned)((tasks + (NT / 64) - 1) / (NT / 64));
+    if (two_four)
+        hipLaunchKernelGGL(transpose_kernel<true>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, wprT, mt);
+    else
+        hipLaunchKernelGGL(transpose_kernel<false>, dim3(blocks), dim3(NT), 0, st, packed, R, (int)C, wpr, wprT, mt);
     return hipGetLastError();
 }
 

@@ -134,10 +134,24 @@ def forward(X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor, 
     return out.view(*lead, R)
 
 
+def workspace_bytes(W: torch.Tensor, B: torch.Tensor, L: int, mask_format=BITMAP) -> int:
+    """Scratch bytes the backward needs (the transposed mask bitmap for bf16)."""
+    R, C = W.shape
+    p = _lib.problem(R, C, L, B.shape[1], 1.0, _dt(W), _fmt(mask_format))
+    n = _lib.workspace_bytes(p)
+    if n == 2**64 - 1:
+        raise ValueError("invalid problem")
+    return n
+
+
 def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor,
              A: torch.Tensor, scale: float, mask_format=BITMAP, need_dx: bool = True,
-             need_dbias: bool = False, out: Optional[Tuple] = None):
-    """(dX, dB, dA, dbias) of the exact, masked gradient; dB/dA/dbias are fp32."""
+             need_dbias: bool = False, out: Optional[Tuple] = None,
+             workspace: Optional[torch.Tensor] = None):
+    """(dX, dB, dA, dbias) of the exact, masked gradient; dB/dA/dbias are fp32.
+
+    ``workspace`` (uint8, at least :func:`workspace_bytes`) is allocated here
+    when not given."""
     X2 = X.reshape(-1, X.shape[-1])
     dY2 = dY.reshape(-1, dY.shape[-1])
     dev = _dev(dY2, X2, W, M, B, A)
@@ -152,9 +166,14 @@ def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor
         dA = torch.empty((r, C), dtype=torch.float32, device=dev)
         dbias = torch.empty(R, dtype=torch.float32, device=dev) if need_dbias else None
     p = _problem(X2, W, B, mask_format, scale)
+    need = _lib.workspace_bytes(p)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    wsb = workspace.numel() if workspace is not None else 0
     with torch.cuda.device(dev):
         _lib.check(_lib.backward(p, _ptr(dY2), _ptr(X2), _ptr(W), _ptr(M), _ptr(B), _ptr(A), _ptr(dX),
-                                 _ptr(dB), _ptr(dA), _ptr(dbias), None, 0, _stream(dev)), "lors_backward")
+                                 _ptr(dB), _ptr(dA), _ptr(dbias), _ptr(workspace), wsb, _stream(dev)),
+                   "lors_backward")
     if dX is not None:
         dX = dX.view(*X.shape)
     return dX, dB, dA, dbias

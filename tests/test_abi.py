@@ -178,7 +178,7 @@ def test_shape(lib, kw):
 
 
 @pytest.mark.parametrize("kw", [dict(R=60), dict(C=36), dict(dtype=_lib.DTYPE_F32, C=66),
-                                dict(flags=_lib.FLAG_BWD_STE)])
+                                dict(flags=_lib.FLAG_BWD_STE), dict(r=5), dict(r=12)])
 def test_unsupported(lib, kw):
     assert _fwd(_p(**kw), _ptrs(6)) == _lib.ERR_UNSUPPORTED
 
@@ -206,8 +206,28 @@ def test_alias(lib):
 
 
 def test_workspace_query(lib):
-    assert _lib.workspace_bytes(_p()) == 0
+    # bf16: transposed mask bitmap, C * ceil(R/32) words, rounded up to 256 B
+    assert _lib.workspace_bytes(_p()) == 512
+    assert _lib.workspace_bytes(_p(R=4096, C=14336)) == 14336 * 128 * 4
+    assert _lib.workspace_bytes(_p(R=520, C=776)) == -(-776 * 17 * 4 // 256) * 256
+    assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32)) == 0
     assert _lib.workspace_bytes(_p(R=0)) == 2**64 - 1
+
+
+def test_workspace_errors(lib):
+    bp = _ptrs(9)
+    dY, X, W, M, B, A, dX, dB, dA = bp
+    ws = BASE + 12 * GAP
+    p = _p()
+    # missing or short workspace
+    assert _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, None, None, 0, None) == _lib.ERR_WORKSPACE
+    assert _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, None, ws, 256, None) == _lib.ERR_WORKSPACE
+    assert _lib.backward_data(p, dY, W, M, B, A, dX, ws, 256, None) == _lib.ERR_WORKSPACE
+    assert _lib.backward_weight(p, dY, X, M, B, A, dB, dA, None, ws, 256, None) == _lib.ERR_WORKSPACE
+    # misaligned or overlapping workspace
+    assert _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, None, ws + 8, 4096, None) == _lib.ERR_ALIGN
+    assert _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, None, dB + 64, 4096, None) == _lib.ERR_ALIAS
+    assert _lib.backward(p, dY, X, W, M, B, A, dX, dB, dA, None, X, 4096, None) == _lib.ERR_ALIAS
 
 
 def test_mask_entry_validation(lib):
