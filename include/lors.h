@@ -112,8 +112,8 @@ typedef enum lors_mask_format {
  * Problem description.
  *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
  *   1 <= r <= 128, every extent < 2^31, scale finite.
- *   bf16: R % 8 == 0, C % 8 == 0 and r % 8 == 0;  fp32: R % 4 == 0 and
- *   C % 4 == 0 (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
+ *   bf16: R % 8 == 0 and C % 8 == 0;  fp32: R % 4 == 0 and C % 4 == 0
+ *   (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
  */
 typedef struct lors_problem {
     int64_t R;

@@ -48,11 +48,27 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _check_no_shared_weak_symbols(objs) -> None:
+    """Fail if two objects define the same weak (template/inline) host symbol
+    from this library's namespace: the linker would keep one definition and
+    silently route both callers to it."""
+    seen = {}
+    for obj in objs:
+        out = subprocess.run(["nm", "--defined-only", obj], capture_output=True, text=True).stdout
+        for line in out.splitlines():
+            parts = line.split()
+            if len(parts) == 3 and parts[1] in ("W", "V") and parts[2].startswith("_ZN4lors"):
+                if parts[2] in seen and seen[parts[2]] != obj:
+                    raise RuntimeError(f"symbol {parts[2]} defined in both {seen[parts[2]]} and {obj}")
+                seen[parts[2]] = obj
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     jobs = min(len(SOURCES), max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))
+    _check_no_shared_weak_symbols(objs)
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -53,8 +53,6 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if ((p->flags & ~LORS_FLAG_REUSE_MASK_T) != 0u) return LORS_ERR_UNSUPPORTED;
     const int64_t row_align = p->dtype == LORS_DTYPE_BF16 ? 8 : 4;
     if (p->R % row_align != 0 || p->C % row_align != 0) return LORS_ERR_UNSUPPORTED;
-    // bf16: rows of B are copied and read 16 bytes at a time.
-    if (p->dtype == LORS_DTYPE_BF16 && p->r % 8 != 0) return LORS_ERR_UNSUPPORTED;
     if (p->dtype == LORS_DTYPE_F32) {
         // The fp32 kernels put token tiles of 64 on the second grid axis.
         if ((p->L + 63) / 64 > 65535 || (p->R + 63) / 64 > 65535) return LORS_ERR_UNSUPPORTED;

@@ -12,6 +12,7 @@
 
 namespace lors {
 namespace wide {
+namespace {  // file-local: both wide kernels have launchers of the same shape
 
 constexpr int BM = 256;  // tokens per tile (GEMM M)
 constexpr int BN = 256;  // output features per tile (GEMM N)
@@ -223,6 +224,7 @@ hipError_t launch_wide(const LayerArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+}  // namespace
 }  // namespace wide
 
 hipError_t launch_fwd_bf16_wide(const LayerArgs& a, hipStream_t st) {

@@ -107,10 +107,8 @@ def test_mask_from_weight(kind):
     (520, 776, 300, 16),    # ragged in every dimension
     (256, 256, 256, 16),    # exactly one tile
     (768, 512, 513, 64),    # r = 64, one token past a tile
-    pytest.param(264, 1032, 77, 5, marks=pytest.mark.skip(
-        reason="bf16 ranks not divisible by 8 are rejected (LORS_ERR_UNSUPPORTED) since this case "
-               "faulted the GPU once with no cause found on the CPU; see the design notes")),
-    (264, 1032, 77, 8),     # smallest rank, short token count
+    (264, 1032, 77, 5),     # odd rank (zero-padded), short token count
+    (264, 1032, 77, 8),     # smallest rank multiple of 8, short token count
     (512, 264, 260, 128),   # largest rank
     (1032, 520, 1, 40),     # single token
 ])
