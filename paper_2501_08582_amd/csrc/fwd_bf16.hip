@@ -5,7 +5,7 @@
 // (Eq. 3 of Section 2.2 and Algorithm 1, with the listing's scale factor.)
 // W' never reaches HBM, and never even reaches LDS: each of the 4 waves owns
 // 64 output features (n) of the 256 x 256 tile and rebuilds exactly those 64
-// rows of W' per K-step in registers, in the operand layout of the main MFMA.
+// rows of W' in registers, in the operand layout of the main MFMA.
 //
 // Merge: the rank-r product T = B.A for a 32(k) x 32(n) block is one
 // 32x32x16 MFMA per 16 ranks whose A operand is A^T with its 32 rows taken in
@@ -16,11 +16,20 @@
 // the select masks for its eight k from a 256-entry LUT indexed by the mask
 // byte, rounds once to bf16, and feeds the MFMA directly.
 //
-// Data movement: X, W and A slabs for a 64-wide K-step are copied from HBM
-// into LDS with global_load_lds (no registers), double-buffered; the mask
-// words come the same way.  Accumulators (256 x 64 per wave) live in AGPRs.
+// Schedule.  A K-step (64 k) is four sub-steps of 16 k.  While the 16 MFMAs
+// of sub-step c run, the wave reads the X fragments of sub-step c+1 and
+// builds its W' fragments; every MFMA slot carries a fixed share of that work
+// (sched_barrier fences), so the matrix pipe never waits for a burst of
+// merge arithmetic.  The rank-r product of the second half of a K-step is
+// formed during sub-step 0.  One barrier per K-step, before sub-step 3:
+// after it the next stage is visible and the current one is free, so
+// sub-step 3 interleaves the copies of stage kt+2 and the first sub-step of
+// stage kt+1 with its MFMAs.  X, W, A and mask slabs travel HBM -> LDS with
+// global_load_lds; accumulators (256 x 64 per wave) live in AGPRs.
 #include "gemm_common.hpp"
 #include "kernels.hpp"
+
+#include <type_traits>
 
 namespace lors {
 namespace {
@@ -30,7 +39,6 @@ constexpr int BM = 256;   // tokens per tile
 constexpr int BN = 256;   // output features per tile (64 per wave)
 constexpr int BK = 64;    // input features per K-step
 constexpr int GROUP_M = 4;
-constexpr int MAXRK = 4;  // ranks up to 64 (wider ranks use the LDS-merge kernel)
 
 constexpr int XB = BM * kRow64;  // 32 KiB
 constexpr int WB = BN * kRow64;  // 32 KiB
@@ -42,13 +50,18 @@ struct Layout {
     static constexpr int X = 0, W = XB, A = XB + WB, M = XB + WB + AB;
     static constexpr int STAGE = XB + WB + AB + MB;
     static constexpr int LUT = 2 * STAGE;         // 256 x 16 B
-    static constexpr int DUMMY = LUT + 4096;      // 1 KiB sink for padding copies
-    static constexpr int TOTAL = DUMMY + 1024;
-    static constexpr int NA = (2 * RK + 3) / 4;   // A-slab copies per wave
-    static constexpr int LOADS = 8 + 8 + NA + 2;  // copies per wave per stage
+    static constexpr int SINK = LUT + 4096;       // 1 KiB target of padding copies
+    static constexpr int TOTAL = SINK + 1024;
+    static constexpr int NAW = (2 * RK + 3) / 4;  // A-slab copies per wave
+    static constexpr int COPIES = 16 + NAW + 2;   // copies per wave per stage
 };
 
-template <int RK, bool TWO_FOUR>
+#define SLOT_END() __builtin_amdgcn_sched_barrier(0)
+
+// RAGGED: some tile reaches past L, R or C (copies then check every lane and
+// read the zero page outside the tensors); otherwise every slab row and
+// K-chunk is in range and copies use a uniform base plus fixed offsets.
+template <int RK, bool TWO_FOUR, bool RAGGED>
 __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
@@ -72,12 +85,12 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const int nk = (C + BK - 1) / BK;
     const int wpr = (C + 31) >> 5;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
-    const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
+    const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * (lane & 7);
 
     // ---- select LUT (visible to all waves after the first stage barrier)
-    // and the resident B operand of the merge
+    // and the resident B operand of the merge: column n = 64 wave + 32 nb + l32,
+    // ranks 16c + 8h .. +7
     *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<TWO_FOUR>((uint32_t)tid);
-
     const bool b_vec = (r & 7) == 0;
     bf16x8 bfr[2][RK];
 #pragma unroll
@@ -101,42 +114,71 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         }
     }
 
-    // ---- asynchronous slab copies for K-step kt into stage st
-    auto issue = [&](int kt, int st) {
-        const int k0 = kt * BK;
-        const uint32_t sb = lds0 + st * Lay::STAGE;
+    // ---- slab copies.  Copy q < 8 of a wave fills slab rows
+    // 8*(8*wave + q) + lane/8 of X (and, copies 8..15, of W); lane l covers
+    // physical chunk l % 8 of its row.  X and W slabs share the offsets.
+    uint32_t offXW[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {      // X and W: 8 rows x 8 chunks per copy
-            const int blk = 8 * wave + q;
+    for (int q = 0; q < 8; ++q) {
+        const int row = 8 * (8 * wave + q) + (lane >> 3);
+        const int lc = (lane & 7) ^ ((row >> 1) & 7);
+        offXW[q] = (uint32_t)((row * C + 8 * lc) * 2);
+    }
+    // A slab: copy q of wave w is slab block 4q + w (rows 8 blk .. +7) when
+    // that block exists; rows at or past r read zeros
+    const uint16_t* aptr[Lay::NAW];
+#pragma unroll
+    for (int q = 0; q < Lay::NAW; ++q) {
+        const int row = 8 * (4 * q + wave) + (lane >> 3);
+        const int lc = (lane & 7) ^ ((row >> 1) & 7);
+        aptr[q] = Am + (int64_t)row * C + 8 * lc;
+    }
+    // mask words [row n][kb]: two 256-byte copies per wave
+    uint32_t offM[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int e = 64 * (2 * wave + q) + lane;
+        offM[q] = (uint32_t)(((e >> 1) * wpr + (e & 1)) * 4);
+    }
+    const uint16_t* Xt = uniform_ptr(X + m0 * C);
+    const uint16_t* Wt = uniform_ptr(W + (int64_t)n0 * C);
+    const uint32_t* Mt = uniform_ptr(Mp + (int64_t)n0 * wpr);
+
+    // copy j of the stage at K offset k0 into the stage at LDS address sb
+    auto copy_j = [&](int j, int k0, uint32_t sb) {
+        if (j < 16) {
+            const int q = j & 7;
+            const bool isx = j < 8;
+            const uint32_t dst = sb + (isx ? Lay::X : Lay::W) + 1024 * (8 * wave + q);
+            if constexpr (!RAGGED) {
+                copy16s_to_lds(uniform_ptr((isx ? Xt : Wt) + k0), offXW[q], dst);
+            } else {
+                const int row = 8 * (8 * wave + q) + (lane >> 3);
+                const int lc = (lane & 7) ^ ((row >> 1) & 7);
+                const bool ok = (isx ? m0 + row < L : n0 + row < R) && k0 + 8 * lc < C;
+                const uint16_t* src = (isx ? Xt : Wt) + (int64_t)row * C + k0 + 8 * lc;
+                copy16_to_lds(ok ? (const void*)src : (const void*)zsrc, dst);
+            }
+        } else if (j < 16 + Lay::NAW) {
+            // every wave issues NAW copies; those past the A slab go to the sink
+            const int q = j - 16, blk = 4 * q + wave;
+            const bool has = blk < 2 * RK;
             const int row = 8 * blk + (lane >> 3);
             const int lc = (lane & 7) ^ ((row >> 1) & 7);
-            const int gk = k0 + 8 * lc;
-            const int64_t gm = m0 + row;
-            const int gn = n0 + row;
-            copy16_to_lds((gm < L && gk < C) ? (const void*)(X + gm * C + gk) : (const void*)zsrc,
-                          sb + Lay::X + 1024 * blk);
-            copy16_to_lds((gn < R && gk < C) ? (const void*)(W + (int64_t)gn * C + gk) : (const void*)zsrc,
-                          sb + Lay::W + 1024 * blk);
-        }
-#pragma unroll
-        for (int q = 0; q < Lay::NA; ++q) {  // A: 16*RK rows; copies beyond go to the sink
-            const int blk = 4 * q + wave;
-            const int row = 8 * blk + (lane >> 3);
-            const int lc = (lane & 7) ^ ((row >> 1) & 7);
-            const int gk = k0 + 8 * lc;
-            const bool real = blk < 2 * RK;
-            const bool ok = real && row < r && gk < C;
-            copy16_to_lds(ok ? (const void*)(Am + (int64_t)row * C + gk) : (const void*)zsrc,
-                          real ? sb + Lay::A + 1024 * blk : lds0 + Lay::DUMMY);
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {      // mask words: [row n][kb]
-            const int e = 64 * (2 * wave + q) + lane;
-            const int row = e >> 1, kb = e & 1;
-            const int gw = (k0 >> 5) + kb;
-            const int gn = n0 + row;
-            copy4_to_lds((gn < R && gw < wpr) ? (const void*)(Mp + (int64_t)gn * wpr + gw) : (const void*)zsrc,
-                         sb + Lay::M + 256 * (2 * wave + q));
+            const bool ok = has && row < r && (!RAGGED || k0 + 8 * lc < C);
+            copy16_to_lds(ok ? (const void*)(aptr[q] + k0) : (const void*)zsrc,
+                          has ? sb + Lay::A + 1024 * blk : lds0 + Lay::SINK);
+        } else {
+            const int q = j - 16 - Lay::NAW;
+            const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
+            if constexpr (!RAGGED) {
+                copy4s_to_lds(uniform_ptr(Mt + (k0 >> 5)), offM[q], dst);
+            } else {
+                const int e = 64 * (2 * wave + q) + lane;
+                const bool ok = n0 + (e >> 1) < R && (k0 >> 5) + (e & 1) < wpr;
+                const uint32_t* src = Mt + (int64_t)(e >> 1) * wpr + (k0 >> 5) + (e & 1);
+                copy4_to_lds(ok ? (const void*)src : (const void*)zsrc, dst);
+            }
         }
     };
 
@@ -156,7 +198,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
                 offAt[kb][t] = Lay::A + slab64_elem_off(row, col);
             }
     }
-    const int nrow[2] = {64 * wave + l32, 64 * wave + 32 + l32};
+    const int nrow0 = 64 * wave + l32;
+    auto xoff = [&](int mb, int c4) { return Lay::X + slab64_off(32 * mb + l32, 2 * c4 + h); };
+    auto woff = [&](int nb, int c4) { return Lay::W + slab64_off(nrow0 + 32 * nb, 2 * c4 + h); };
 
     f32x16 acc[8][2];
 #pragma unroll
@@ -166,66 +210,126 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    issue(0, 0);
-    if (nk > 1) issue(1, 1);
+    bf16x8 xa[8], xb[8];      // X fragments of alternate sub-steps
+    u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
+    f32x16 T[2];              // rank-r block of the current 32-wide k half
+    uint32_t mw[2][2];        // mask words [nb][kb] of the current K-step
+    u32x4 raw[2], sel[2];     // W and select masks of the sub-step being merged
+    bf16x8 afr[RK];
 
+    auto mm = [&](int i, const bf16x8 (&xf)[8], const u32x4 (&wf)[2]) {
+        const int mb = i >> 1, nb = i & 1;
+        acc[mb][nb] = mfma_32x32x16(xf[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+    };
+    auto read_afr = [&](const uint8_t* sb, int kb) {
+#pragma unroll
+        for (int c = 0; c < RK; ++c)
+            afr[c] = frag_from_tr(lds_tr_read(sb + offAt[kb][0] + 16 * kRow64 * c),
+                                  lds_tr_read(sb + offAt[kb][1] + 16 * kRow64 * c));
+    };
+    auto read_mw = [&](const uint8_t* sb) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const u32x2 v = *(const u32x2*)(sb + Lay::M + 8 * (nrow0 + 32 * nb));
+            mw[nb][0] = v[0];
+            mw[nb][1] = v[1];
+        }
+    };
+    // raw W and select masks of sub-step c4 of the stage at sb
+    auto read_rs = [&](const uint8_t* sb, int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            raw[nb] = *(const u32x4*)(sb + woff(nb, c4));
+            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
+            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+        }
+    };
+    auto read_x2 = [&](bf16x8 (&xf)[8], const uint8_t* sb, int c4, int p) {
+        xf[2 * p] = *(const bf16x8*)(sb + xoff(2 * p, c4));
+        xf[2 * p + 1] = *(const bf16x8*)(sb + xoff(2 * p + 1, c4));
+    };
+    // merge piece p (0..7): pair p % 4 of fragment nb = p / 4, T half cp
+    auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
+        const int nb = p >> 2, q = p & 3;
+        wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
+    };
+    // an ordinary sub-step: MFMAs on (xc, wc) while preparing (xn, wn) for
+    // sub-step c4n of the stage at sb; optionally the rank-r block of k half 1
+    auto substep = [&](const bf16x8 (&xc)[8], const u32x4 (&wc)[2], bf16x8 (&xn)[8], u32x4 (&wn)[2],
+                       const uint8_t* sb, int c4n, auto rank_tag) {
+        constexpr bool RANK = decltype(rank_tag)::value;
+        mm(0, xc, wc); read_rs(sb, c4n); SLOT_END();
+        mm(1, xc, wc); if constexpr (RANK) read_afr(sb, 1); SLOT_END();
+        mm(2, xc, wc); read_x2(xn, sb, c4n, 0); SLOT_END();
+        mm(3, xc, wc); read_x2(xn, sb, c4n, 1); SLOT_END();
+        mm(4, xc, wc); read_x2(xn, sb, c4n, 2); SLOT_END();
+        mm(5, xc, wc); read_x2(xn, sb, c4n, 3); SLOT_END();
+        mm(6, xc, wc); SLOT_END();
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, xc, wc);
+            merge_piece(wn, p, c4n & 1);
+            SLOT_END();
+        }
+        mm(15, xc, wc);
+        if constexpr (RANK) rank_mfma2<RK>(T, afr, bfr);  // after the merge pieces read T
+        SLOT_END();
+    };
+
+    // ---- prologue: stages 0 and 1 in flight, then sub-step 0 of stage 0
+#pragma unroll
+    for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
+#pragma unroll
+    for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, nk > 1 ? BK : 0, lds0 + Lay::STAGE);
+    stage_barrier<0>();
+    read_mw(smem);
+    read_afr(smem, 0);
+    rank_mfma2<RK>(T, afr, bfr);
+    read_rs(smem, 0);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) read_x2(xa, smem, 0, p);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) merge_piece(wa, p, 0);
+
+    // ---- main loop (no data-dependent branches: at the tail the copies
+    // repeat the last K-slab into the buffer just consumed, and the reads of
+    // the "next" stage after the last K-step are never used)
     for (int kt = 0; kt < nk; ++kt) {
         const int st = kt & 1;
-        if (kt + 1 < nk)
-            stage_barrier<Lay::LOADS>();
-        else
-            stage_barrier<0>();
         const uint8_t* sb = smem + st * Lay::STAGE;
-
+        const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
+        substep(xa, wa, xb, wb, sb, 1, std::true_type{});
+        substep(xb, wb, xa, wa, sb, 2, std::false_type{});
+        substep(xa, wa, xb, wb, sb, 3, std::false_type{});
+        // sub-step 3: stage kt+1 landed everywhere, stage kt free
+        stage_barrier<0>();
+        const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
+        const uint32_t sq = lds0 + st * Lay::STAGE;
+        mm(0, xb, wb); read_mw(sn); read_afr(sn, 0); copy_j(0, k2, sq); SLOT_END();
+        mm(1, xb, wb); copy_j(1, k2, sq); copy_j(2, k2, sq); SLOT_END();
+        mm(2, xb, wb); read_x2(xa, sn, 0, 0); copy_j(3, k2, sq); copy_j(4, k2, sq); SLOT_END();
+        mm(3, xb, wb); read_x2(xa, sn, 0, 1); copy_j(5, k2, sq); copy_j(6, k2, sq); SLOT_END();
+        mm(4, xb, wb); read_rs(sn, 0); copy_j(7, k2, sq); copy_j(8, k2, sq); SLOT_END();
+        mm(5, xb, wb); read_x2(xa, sn, 0, 2); copy_j(9, k2, sq); copy_j(10, k2, sq); SLOT_END();
+        mm(6, xb, wb); read_x2(xa, sn, 0, 3); rank_mfma2<RK>(T, afr, bfr); copy_j(11, k2, sq); SLOT_END();
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            // A^T fragments for this 32-wide half of the K-step
-            bf16x8 afr[RK];
-#pragma unroll
-            for (int c = 0; c < RK; ++c)
-                afr[c] = frag_from_tr(lds_tr_read(sb + offAt[kb][0] + 16 * kRow64 * c),
-                                      lds_tr_read(sb + offAt[kb][1] + 16 * kRow64 * c));
-            bf16x8 wf[2][2];  // [nb][c'] merged W' fragments for chunks 2kb + c'
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                f32x16 T;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) T[v] = 0.f;
-#pragma unroll
-                for (int c = 0; c < RK; ++c) T = mfma_32x32x16(afr[c], bfr[nb][c], T);
-                const uint32_t word = *(const uint32_t*)(sb + Lay::M + 8 * nrow[nb] + 4 * kb);
-#pragma unroll
-                for (int cp = 0; cp < 2; ++cp) {
-                    const u32x4 raw = *(const u32x4*)(sb + Lay::W + slab64_off(nrow[nb], 4 * kb + 2 * cp + h));
-                    const uint32_t byte = (word >> (8 * (2 * cp + h))) & 0xFFu;
-                    const u32x4 sel = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
-                    float t8[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) t8[e] = T[8 * cp + e];
-                    wf[nb][cp] = as_bf16x8(merge8(raw, t8, s, sel));
-                }
-            }
-#pragma unroll
-            for (int cp = 0; cp < 2; ++cp) {
-                const int c4 = 2 * kb + cp;
-                bf16x8 xf[8];
-#pragma unroll
-                for (int mb = 0; mb < 8; ++mb)
-                    xf[mb] = *(const bf16x8*)(sb + Lay::X + slab64_off(32 * mb + l32, 2 * c4 + h));
-#pragma unroll
-                for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(xf[mb], wf[nb][cp], acc[mb][nb]);
-            }
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, xb, wb);
+            merge_piece(wa, p, 0);
+            if (12 + p < Lay::COPIES) copy_j(12 + p, k2, sq);
+            SLOT_END();
         }
-        lds_barrier();
-        if (kt + 2 < nk) issue(kt + 2, st);
+        mm(15, xb, wb);
+#pragma unroll
+        for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
+        SLOT_END();
     }
+    wait_vmcnt<0>();
 
     // ---- epilogue: (+bias), round to bf16, store
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        const int gn = n0 + nrow[nb];
+        const int gn = n0 + nrow0 + 32 * nb;
         if (gn >= R) continue;
         const float bv = bias ? bf16_bits_to_f32(bias[gn]) : 0.f;
 #pragma unroll
@@ -239,8 +343,8 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     }
 }
 
-template <int RK>
-hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
+template <int RK, bool TWO_FOUR>
+hipError_t launch_fmt(const LayerArgs& a, hipStream_t st) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.R + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
@@ -250,13 +354,22 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     auto* A = (const uint16_t*)a.A;
     auto* bias = (const uint16_t*)a.bias;
     auto* Y = (uint16_t*)a.Y;
-    if (a.two_four)
-        hipLaunchKernelGGL((fwd_kernel<RK, true>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
+    // the fixed-offset copies need every tile and K-step in range and the
+    // per-lane byte offsets (256 slab rows of C bf16 or of the mask) inside
+    // 32 bits
+    const bool ragged = a.L % BM != 0 || a.R % BN != 0 || a.C % BK != 0 || (int64_t)BM * a.C * 2 >= (1ll << 31);
+    if (ragged)
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
                            (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     else
-        hipLaunchKernelGGL((fwd_kernel<RK, false>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
                            (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
+}
+
+template <int RK>
+hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
+    return a.two_four ? launch_fmt<RK, true>(a, st) : launch_fmt<RK, false>(a, st);
 }
 
 }  // namespace

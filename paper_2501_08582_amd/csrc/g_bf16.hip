@@ -67,27 +67,25 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const int64_t nk = (L + BK - 1) / BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
 
-    // ---- asynchronous slab copies: copy q of this wave fills tile rows
-    // 2*(8*wave + q) + {0, 1}; lane l covers physical chunk l % 32 of its row.
+    // ---- asynchronous slab copies: copy pair q of this wave fills tile row
+    // 2*(8*wave + q) + h of the dY slab and of the X slab; lane l covers
+    // physical chunk l % 32 of its row.  Rows past L and columns past R / C
+    // read the zero page.
     const int pchunk = lane & 31;
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
-    auto issue = [&](int64_t kt, int st) {
-        const uint32_t sb = lds0 + st * STAGEB;
-#pragma unroll
-        for (int q = 0; q < LOADS; ++q) {
-            const int row = 2 * (LOADS * wave + q) + h;
-            const int lc = swz_chunk(row, pchunk);
-            const int64_t gl = kt * BK + row;
-            const int gi = i0 + lc * 8, gj = j0 + lc * 8;
-            const void* a = (gl < L && gi < R) ? (const void*)(dY + gl * R + gi) : (const void*)zsrc;
-            const void* b = (gl < L && gj < C) ? (const void*)(X + gl * C + gj) : (const void*)zsrc;
-            copy16_to_lds(a, sb + (LOADS * wave + q) * 1024);
-            copy16_to_lds(b, sb + TILEB + (LOADS * wave + q) * 1024);
-        }
+    auto copy_pair = [&](int q, int64_t k0, uint32_t sb) {
+        const int row = 2 * (LOADS * wave + q) + h;
+        const int lc = swz_chunk(row, pchunk);
+        const int64_t gl = k0 + row;
+        const int gi = i0 + lc * 8, gj = j0 + lc * 8;
+        const void* a = (gl < L && gi < R) ? (const void*)(dY + gl * R + gi) : (const void*)zsrc;
+        const void* b = (gl < L && gj < C) ? (const void*)(X + gl * C + gj) : (const void*)zsrc;
+        copy16_to_lds(a, sb + (LOADS * wave + q) * 1024);
+        copy16_to_lds(b, sb + TILEB + (LOADS * wave + q) * 1024);
     };
 
-    // Per-lane fragment offsets inside a slab (stage and chunk added later).
+    // Per-lane fragment offsets inside a stage (sub-step rows added later).
     int offA[4][2], offB[4][2];
 #pragma unroll
     for (int b = 0; b < 4; ++b)
@@ -96,6 +94,15 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
             offA[b][t] = tr_frag_off(lane, 0, wi * 128 + 32 * b, t);
             offB[b][t] = TILEB + tr_frag_off(lane, 0, wj * 128 + 32 * b, t);
         }
+    auto load_frags = [&](bf16x8 (&fa)[4], bf16x8 (&fb)[4], const uint8_t* base, int c) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            fa[b] = frag_from_tr(lds_tr_read(base + 16 * c * kRowBytes + offA[b][0]),
+                                 lds_tr_read(base + 16 * c * kRowBytes + offA[b][1]));
+            fb[b] = frag_from_tr(lds_tr_read(base + 16 * c * kRowBytes + offB[b][0]),
+                                 lds_tr_read(base + 16 * c * kRowBytes + offB[b][1]));
+        }
+    };
 
     f32x16 acc[4][4];
 #pragma unroll
@@ -105,31 +112,63 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
 
-    if (nk > 0) issue(0, 0);
-    if (nk > 1) issue(1, 1);
+    // ---- main loop.  Software pipeline: the operand fragments of sub-step
+    // c+1 are read from LDS while the 16 MFMAs of sub-step c run.  One
+    // barrier per K-step, before its last sub-step: after it every wave has
+    // finished reading the current stage and the next stage has landed, so
+    // the last sub-step interleaves its MFMAs with the copies of stage kt+2
+    // (into the buffer just consumed) and the first fragment reads of stage
+    // kt+1.  The body has no data-dependent branches: at the tail the copies
+    // repeat the last K-slab into a buffer that is never read again.
+    static_assert(BK / 16 == 4 && LOADS == 8, "sub-step schedule below assumes 4 sub-steps, 8 copy pairs");
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+        const int64_t k0 = (int64_t)(st < nk ? st : nk - 1) * BK;
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) copy_pair(q, k0, lds0 + st * STAGEB);
+    }
+    stage_barrier<2 * LOADS>();  // stage 0 landed everywhere; stage 1 may still fly
+
+    bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+    load_frags(fa0, fb0, smem, 0);
+    auto mfma16 = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) acc[a][b] = mfma_32x32x16(fa[a], fb[b], acc[a][b]);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+        }
+    };
     for (int64_t kt = 0; kt < nk; ++kt) {
         const int st = (int)(kt & 1);
-        if (kt + 1 < nk)
-            stage_barrier<2 * LOADS>();  // this stage landed; the next may still fly
-        else
-            stage_barrier<0>();
         const uint8_t* sb = smem + st * STAGEB;
+        const uint8_t* sn = smem + (st ^ 1) * STAGEB;
+        load_frags(fa1, fb1, sb, 1);
+        mfma16(fa0, fb0);
+        load_frags(fa0, fb0, sb, 2);
+        mfma16(fa1, fb1);
+        load_frags(fa1, fb1, sb, 3);
+        mfma16(fa0, fb0);
+        stage_barrier<0>();
+        const int64_t k0 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
+        const uint32_t sbq = lds0 + st * STAGEB;
 #pragma unroll
-        for (int c = 0; c < BK / 16; ++c) {
-            const int rowoff = 16 * c * kRowBytes;  // 16 rows further (swizzle period 4 divides 16)
-            bf16x8 fa[4], fb[4];
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                fa[b] = frag_from_tr(lds_tr_read(sb + rowoff + offA[b][0]), lds_tr_read(sb + rowoff + offA[b][1]));
-                fb[b] = frag_from_tr(lds_tr_read(sb + rowoff + offB[b][0]), lds_tr_read(sb + rowoff + offB[b][1]));
+        for (int i = 0; i < 16; ++i) {
+            const int a = i >> 2, b = i & 3;
+            acc[a][b] = mfma_32x32x16(fa1[a], fb1[b], acc[a][b]);
+            if ((i & 1) == 0) copy_pair(i >> 1, k0, sbq);
+            if (i < 8) {
+                // fragment i/2 of A (even i) or B (odd i) of sub-step 0, stage kt+1
+                if ((i & 1) == 0)
+                    fa0[i >> 1] = frag_from_tr(lds_tr_read(sn + offA[i >> 1][0]), lds_tr_read(sn + offA[i >> 1][1]));
+                else
+                    fb0[i >> 1] = frag_from_tr(lds_tr_read(sn + offB[i >> 1][0]), lds_tr_read(sn + offB[i >> 1][1]));
             }
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < 4; ++b) acc[a][b] = mfma_32x32x16(fa[a], fb[b], acc[a][b]);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        lds_barrier();  // every wave is done reading this stage
-        if (kt + 2 < nk) issue(kt + 2, st);
     }
     stage_barrier<0>();
 

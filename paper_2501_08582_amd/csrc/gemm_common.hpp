@@ -49,7 +49,6 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_wave
                  : "v"(src), "s"(lds_wave_base)
                  : "memory", "m0");
 }
-#pragma clang diagnostic pop
 
 // ---------------------------------------------------------------------------
 // Slabs with 64 bf16 (128 bytes) per row, read one 16-byte chunk per lane
@@ -108,6 +107,66 @@ __device__ __forceinline__ void copy4_to_lds(const void* src, uint32_t lds_wave_
                  : "memory", "m0");
 }
 
+// A wave-uniform pointer moved into scalar registers (the copies below take
+// their base address from an SGPR pair).
+template <typename T>
+__device__ __forceinline__ const T* uniform_ptr(const T* p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const T*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+// The same copies addressed as a wave-uniform base (SGPR pair) plus a 32-bit
+// per-lane byte offset: no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void copy16s_to_lds(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(sbase), "s"(lds_wave_base)
+                 : "memory", "m0");
+}
+__device__ __forceinline__ void copy4s_to_lds(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+                 :
+                 : "v"(voff), "s"(sbase), "s"(lds_wave_base)
+                 : "memory", "m0");
+}
+
+// T[nb] = sum over c of mfma(a[c], b[nb][c]) for nb = 0, 1, with T in VGPRs.
+// The main accumulators fill the accumulation registers, so results that the
+// VALU consumes are produced by inline-assembly MFMAs writing VGPRs directly
+// (chained accumulation into the same registers needs no wait states).  The
+// final s_nop block covers the matrix-result -> VALU-read latency; it also
+// keeps the A fragments allocated until the matrix core has consumed them.
+template <int RK>
+__device__ __forceinline__ void rank_mfma2(f32x16 (&T)[2], const bf16x8 (&a)[RK], const bf16x8 (&b)[2][RK]) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(T[nb]) : "v"(a[0]), "v"(b[nb][0]));
+#pragma unroll
+        for (int c = 1; c < RK; ++c)
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[c]), "v"(b[nb][c]));
+    }
+    if constexpr (RK == 1)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]));
+    else if constexpr (RK == 2)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]));
+    else if constexpr (RK == 3)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
+    else {
+        static_assert(RK == 4, "ranks up to 64");
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2"
+                     : "+v"(T[0]), "+v"(T[1])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+    }
+}
+
+// One bf16 pair of W' = select(M, W + s.T, 0): raw holds the two bf16 of W,
+// t0/t1 the rank-r sums, sel the 32-bit select mask of the pair.
+__device__ __forceinline__ uint32_t merge_pair(uint32_t raw, float t0, float t1, float s, uint32_t sel) {
+    return pack_bf16x2(fmaf(s, t0, __uint_as_float(raw << 16)), fmaf(s, t1, __uint_as_float(raw & 0xFFFF0000u))) & sel;
+}
+
 // Wait until at most N of this wave's vector-memory loads (including the
 // LDS copies above) are outstanding, then barrier: afterwards every copy
 // issued before the last N of every wave is visible in LDS.
@@ -158,5 +217,7 @@ __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+
+#pragma clang diagnostic pop
 
 }  // namespace lors

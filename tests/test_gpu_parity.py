@@ -106,6 +106,7 @@ def test_mask_from_weight(kind):
 @pytest.mark.parametrize("R,C,L,r", [
     (520, 776, 300, 16),    # ragged in every dimension
     (256, 256, 256, 16),    # exactly one tile
+    (512, 768, 512, 48),    # whole tiles in every dimension (fixed-offset copies), r = 48
     (768, 512, 513, 64),    # r = 64, one token past a tile
     (264, 1032, 77, 5),     # odd rank (zero-padded), short token count
     (264, 1032, 77, 8),     # smallest rank multiple of 8, short token count
@@ -117,7 +118,8 @@ def test_parity_bitmap(R, C, L, r):
     _check_all(inp)
 
 
-@pytest.mark.parametrize("R,C,L,r", [(520, 776, 300, 16), (1024, 512, 700, 64)])
+@pytest.mark.parametrize("R,C,L,r", [(520, 776, 300, 16), (1024, 512, 700, 64),
+                                     (512, 512, 256, 64)])  # whole tiles, r = 64
 def test_parity_two_four(R, C, L, r):
     inp = _inputs("llama2_7b_up_proj_2_4", R=R, C=C, L=L, r=r, seed=7 * R + L)
     _check_all(inp)
