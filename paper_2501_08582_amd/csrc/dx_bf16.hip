@@ -15,9 +15,15 @@
 //     contiguously into LDS each K-step; A[:, n] is resident in registers;
 //   * the mask bits a lane needs run along k for a fixed n, so they are read
 //     from the transposed bitmap M^T (built once per backward call).
+// The schedule is the forward's: four sub-steps of 16 k per K-step, each
+// MFMA slot carrying a fixed share of the next sub-step's operand reads and
+// merge arithmetic, one barrier per K-step before the last sub-step, which
+// interleaves the copies of stage kt+2 and the first sub-step of stage kt+1.
 // Requires r % 8 == 0 and r <= 64 (other ranks use the LDS-merge kernel).
 #include "gemm_common.hpp"
 #include "kernels.hpp"
+
+#include <type_traits>
 
 namespace lors {
 namespace {
@@ -38,13 +44,18 @@ struct Layout {
     static constexpr int D = 0, W = DB, B = DB + WB, M = DB + WB + BB;
     static constexpr int STAGE = DB + WB + BB + MB;
     static constexpr int LUT = 2 * STAGE;
-    static constexpr int DUMMY = LUT + 4096;
-    static constexpr int TOTAL = DUMMY + 1024;
+    static constexpr int SINK = LUT + 4096;        // 1 KiB target of padding copies
+    static constexpr int TOTAL = SINK + 1024;
     static constexpr int NB = (2 * RK + 3) / 4;    // B-slab copies per wave (r/8 copies in all)
-    static constexpr int LOADS = 8 + 8 + NB + 2;
+    static constexpr int COPIES = 16 + NB + 2;     // copies per wave per stage
 };
 
-template <int RK, bool TWO_FOUR_UNUSED>
+#define SLOT_END() __builtin_amdgcn_sched_barrier(0)
+
+// RAGGED: some tile reaches past L, C or R (copies check every lane and read
+// the zero page outside the tensors); otherwise copies use uniform bases plus
+// fixed per-lane offsets.
+template <int RK, bool RAGGED>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
@@ -96,52 +107,84 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                                       lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
     lds_barrier();
 
-    auto issue = [&](int kt, int st) {
-        const int k0 = kt * BK;
-        const uint32_t sb = lds0 + st * Lay::STAGE;
+    // ---- slab copies.  Copies 0..7: dY slab rows 8*(8*wave + q) + lane/8
+    // (64 k per row); copies 8..15: W slab rows 2*(8*wave + q) + h (256 n
+    // per row); then the B slab (one contiguous block) and the M^T words.
+    uint32_t offD[8], offW[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int blk = 8 * wave + q;
-            {   // dY slab: rows m, 64 k per row
+    for (int q = 0; q < 8; ++q) {
+        const int blk = 8 * wave + q;
+        const int rd = 8 * blk + (lane >> 3);
+        offD[q] = (uint32_t)((rd * R + 8 * ((lane & 7) ^ ((rd >> 1) & 7))) * 2);
+        const int rw = 2 * blk + h;
+        offW[q] = (uint32_t)((rw * C + 8 * swz_chunk(rw, lane & 31)) * 2);
+    }
+    uint32_t offM[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int e = 64 * (2 * wave + q) + lane;
+        offM[q] = (uint32_t)(((e >> 1) * wprT + (e & 1)) * 4);
+    }
+    const uint16_t* Dt = uniform_ptr(dY + m0 * R);
+    const uint16_t* Wn = uniform_ptr(W + n0);
+    const uint32_t* Mn = uniform_ptr(Mt + (int64_t)n0 * wprT);
+
+    auto copy_j = [&](int j, int k0, uint32_t sb) {
+        if (j < 8) {
+            const int q = j, blk = 8 * wave + q;
+            const uint32_t dst = sb + Lay::D + 1024 * blk;
+            if constexpr (!RAGGED) {
+                copy16s_to_lds(uniform_ptr(Dt + k0), offD[q], dst);
+            } else {
                 const int row = 8 * blk + (lane >> 3);
                 const int lc = (lane & 7) ^ ((row >> 1) & 7);
-                const int gk = k0 + 8 * lc;
-                const int64_t gm = m0 + row;
-                copy16_to_lds((gm < L && gk < R) ? (const void*)(dY + gm * R + gk) : (const void*)zsrc,
-                              sb + Lay::D + 1024 * blk);
+                const bool ok = m0 + row < L && k0 + 8 * lc < R;
+                copy16_to_lds(ok ? (const void*)(Dt + (int64_t)row * R + k0 + 8 * lc) : (const void*)zsrc, dst);
             }
-            {   // W slab: rows k, 256 n per row
+        } else if (j < 16) {
+            const int q = j - 8, blk = 8 * wave + q;
+            const uint32_t dst = sb + Lay::W + 1024 * blk;
+            if constexpr (!RAGGED) {
+                copy16s_to_lds(uniform_ptr(Wn + (int64_t)k0 * C), offW[q], dst);
+            } else {
                 const int row = 2 * blk + h;
                 const int lc = swz_chunk(row, lane & 31);
-                const int gk = k0 + row, gn = n0 + 8 * lc;
-                copy16_to_lds((gk < R && gn < C) ? (const void*)(W + (int64_t)gk * C + gn) : (const void*)zsrc,
-                              sb + Lay::W + 1024 * blk);
+                const bool ok = k0 + row < R && n0 + 8 * lc < C;
+                copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + 8 * lc) : (const void*)zsrc, dst);
             }
-        }
-#pragma unroll
-        for (int q = 0; q < Lay::NB; ++q) {  // B rows k0 .. k0+63: one contiguous block
-            const int blk = 4 * q + wave;
+        } else if (j < 16 + Lay::NB) {
+            // B rows k0 .. k0+63 are one contiguous block; every wave issues
+            // NB copies, those past the block go to the sink
+            const int blk = 4 * (j - 16) + wave;
             const bool real = blk < nbcopies;
             const int off = 1024 * blk + 16 * lane;   // byte offset inside the slab
-            const bool ok = real && k0 + off / slab_b < R;
+            const bool ok = real && (!RAGGED || k0 + off / slab_b < R);
             copy16_to_lds(ok ? (const void*)((const uint8_t*)Bm + (int64_t)k0 * slab_b + off) : (const void*)zsrc,
-                          real ? sb + Lay::B + 1024 * blk : lds0 + Lay::DUMMY);
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {      // M^T words: [n][kb]
-            const int e = 64 * (2 * wave + q) + lane;
-            const int n = e >> 1, kb = e & 1;
-            const int gw = (k0 >> 5) + kb;
-            const int gn = n0 + n;
-            copy4_to_lds((gn < C && gw < wprT) ? (const void*)(Mt + (int64_t)gn * wprT + gw) : (const void*)zsrc,
-                         sb + Lay::M + 256 * (2 * wave + q));
+                          real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
+        } else {
+            const int q = j - 16 - Lay::NB;
+            const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
+            if constexpr (!RAGGED) {
+                copy4s_to_lds(uniform_ptr(Mn + (k0 >> 5)), offM[q], dst);
+            } else {
+                const int e = 64 * (2 * wave + q) + lane;
+                const int n = e >> 1, gw = (k0 >> 5) + (e & 1);
+                const bool ok = n0 + n < C && gw < wprT;
+                copy4_to_lds(ok ? (const void*)(Mn + (int64_t)n * wprT + gw) : (const void*)zsrc, dst);
+            }
         }
     };
 
     // Rows of the merge A operand: lane (rho = l32, h) reads B row pi(rho).
     const int rho = l32;
     const int pik = 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho >> 3) & 1) + (rho & 3);
-    const int ncol[2] = {64 * wave + l32, 64 * wave + 32 + l32};
+    const int ncol0 = 64 * wave + l32;
+    int offWt[2][2];  // transpose-read offsets of the raw W fragments, sub-step row 0
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) offWt[nb][t] = Lay::W + tr_frag_off(lane, 0, 64 * wave + 32 * nb, t);
+    auto doff = [&](int mb, int c4) { return Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h); };
 
     f32x16 acc[8][2];
 #pragma unroll
@@ -151,71 +194,126 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    issue(0, 0);
-    if (nk > 1) issue(1, 1);
+    bf16x8 da[8], db[8];      // dY fragments of alternate sub-steps
+    u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
+    f32x16 T[2];              // rank-r block of the current 32-wide k half
+    uint32_t mw[2][2];        // M^T words [nb][kb] of the current K-step
+    u32x4 raw[2], sel[2];
+    bf16x8 bfr[RK];           // B[32kb + pi(rho)][16c + 8h .. +7]
 
+    auto mm = [&](int i, const bf16x8 (&df)[8], const u32x4 (&wf)[2]) {
+        const int mb = i >> 1, nb = i & 1;
+        acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+    };
+    auto read_bfr = [&](const uint8_t* sb, int kb) {
+#pragma unroll
+        for (int c = 0; c < RK; ++c) {
+            const int j0 = 16 * c + 8 * h;
+            u32x4 v = zero_u32x4();
+            if (j0 < r) v = *(const u32x4*)(sb + Lay::B + (32 * kb + pik) * slab_b + 2 * j0);
+            bfr[c] = as_bf16x8(v);
+        }
+    };
+    auto read_mw = [&](const uint8_t* sb) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const u32x2 v = *(const u32x2*)(sb + Lay::M + 8 * (ncol0 + 32 * nb));
+            mw[nb][0] = v[0];
+            mw[nb][1] = v[1];
+        }
+    };
+    auto read_rs = [&](const uint8_t* sb, int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRowBytes);
+            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRowBytes);
+            raw[nb][0] = lo[0];
+            raw[nb][1] = lo[1];
+            raw[nb][2] = hi[0];
+            raw[nb][3] = hi[1];
+            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
+            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+        }
+    };
+    auto read_d2 = [&](bf16x8 (&df)[8], const uint8_t* sb, int c4, int p) {
+        df[2 * p] = *(const bf16x8*)(sb + doff(2 * p, c4));
+        df[2 * p + 1] = *(const bf16x8*)(sb + doff(2 * p + 1, c4));
+    };
+    auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
+        const int nb = p >> 2, q = p & 3;
+        wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
+    };
+    auto substep = [&](const bf16x8 (&dc)[8], const u32x4 (&wc)[2], bf16x8 (&dn)[8], u32x4 (&wn)[2],
+                       const uint8_t* sb, int c4n, auto rank_tag) {
+        constexpr bool RANK = decltype(rank_tag)::value;
+        mm(0, dc, wc); read_rs(sb, c4n); SLOT_END();
+        mm(1, dc, wc); if constexpr (RANK) read_bfr(sb, 1); SLOT_END();
+        mm(2, dc, wc); read_d2(dn, sb, c4n, 0); SLOT_END();
+        mm(3, dc, wc); read_d2(dn, sb, c4n, 1); SLOT_END();
+        mm(4, dc, wc); read_d2(dn, sb, c4n, 2); SLOT_END();
+        mm(5, dc, wc); read_d2(dn, sb, c4n, 3); SLOT_END();
+        mm(6, dc, wc); SLOT_END();
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, dc, wc);
+            merge_piece(wn, p, c4n & 1);
+            SLOT_END();
+        }
+        mm(15, dc, wc);
+        if constexpr (RANK) rank_mfma2<RK>(T, bfr, afr);  // after the merge pieces read T
+        SLOT_END();
+    };
+
+    // ---- prologue: stages 0 and 1 in flight, then sub-step 0 of stage 0
+#pragma unroll
+    for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
+#pragma unroll
+    for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, nk > 1 ? BK : 0, lds0 + Lay::STAGE);
+    stage_barrier<0>();
+    read_mw(smem);
+    read_bfr(smem, 0);
+    rank_mfma2<RK>(T, bfr, afr);
+    read_rs(smem, 0);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) read_d2(da, smem, 0, p);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) merge_piece(wa, p, 0);
+
+    // ---- main loop (branch-free, see the forward kernel)
     for (int kt = 0; kt < nk; ++kt) {
         const int st = kt & 1;
-        if (kt + 1 < nk)
-            stage_barrier<Lay::LOADS>();
-        else
-            stage_barrier<0>();
         const uint8_t* sb = smem + st * Lay::STAGE;
-
+        const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
+        substep(da, wa, db, wb, sb, 1, std::true_type{});
+        substep(db, wb, da, wa, sb, 2, std::false_type{});
+        substep(da, wa, db, wb, sb, 3, std::false_type{});
+        stage_barrier<0>();
+        const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
+        const uint32_t sq = lds0 + st * Lay::STAGE;
+        mm(0, db, wb); read_mw(sn); read_bfr(sn, 0); copy_j(0, k2, sq); SLOT_END();
+        mm(1, db, wb); copy_j(1, k2, sq); copy_j(2, k2, sq); SLOT_END();
+        mm(2, db, wb); read_d2(da, sn, 0, 0); copy_j(3, k2, sq); copy_j(4, k2, sq); SLOT_END();
+        mm(3, db, wb); read_d2(da, sn, 0, 1); copy_j(5, k2, sq); copy_j(6, k2, sq); SLOT_END();
+        mm(4, db, wb); read_rs(sn, 0); copy_j(7, k2, sq); copy_j(8, k2, sq); SLOT_END();
+        mm(5, db, wb); read_d2(da, sn, 0, 2); copy_j(9, k2, sq); copy_j(10, k2, sq); SLOT_END();
+        mm(6, db, wb); read_d2(da, sn, 0, 3); rank_mfma2<RK>(T, bfr, afr); copy_j(11, k2, sq); SLOT_END();
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            bf16x8 bfr[RK];  // B[32kb + pi(rho)][16c + 8h .. +7]
-#pragma unroll
-            for (int c = 0; c < RK; ++c) {
-                const int j0 = 16 * c + 8 * h;
-                u32x4 v = zero_u32x4();
-                if (j0 < r) v = *(const u32x4*)(sb + Lay::B + (32 * kb + pik) * slab_b + 2 * j0);
-                bfr[c] = as_bf16x8(v);
-            }
-            bf16x8 wf[2][2];
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                f32x16 T;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) T[v] = 0.f;
-#pragma unroll
-                for (int c = 0; c < RK; ++c) T = mfma_32x32x16(bfr[c], afr[nb][c], T);
-                const uint32_t word = *(const uint32_t*)(sb + Lay::M + 8 * ncol[nb] + 4 * kb);
-#pragma unroll
-                for (int cp = 0; cp < 2; ++cp) {
-                    const int row0 = 32 * kb + 16 * cp;
-                    const u32x2 lo = lds_tr_read(sb + Lay::W + tr_frag_off(lane, row0, 64 * wave + 32 * nb, 0));
-                    const u32x2 hi = lds_tr_read(sb + Lay::W + tr_frag_off(lane, row0, 64 * wave + 32 * nb, 1));
-                    u32x4 raw;
-                    raw[0] = lo[0]; raw[1] = lo[1]; raw[2] = hi[0]; raw[3] = hi[1];
-                    const uint32_t byte = (word >> (8 * (2 * cp + h))) & 0xFFu;
-                    const u32x4 sel = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
-                    float t8[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) t8[e] = T[8 * cp + e];
-                    wf[nb][cp] = as_bf16x8(merge8(raw, t8, s, sel));
-                }
-            }
-#pragma unroll
-            for (int cp = 0; cp < 2; ++cp) {
-                const int c4 = 2 * kb + cp;
-                bf16x8 df[8];
-#pragma unroll
-                for (int mb = 0; mb < 8; ++mb)
-                    df[mb] = *(const bf16x8*)(sb + Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h));
-#pragma unroll
-                for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_32x32x16(df[mb], wf[nb][cp], acc[mb][nb]);
-            }
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, db, wb);
+            merge_piece(wa, p, 0);
+            if (12 + p < Lay::COPIES) copy_j(12 + p, k2, sq);
+            SLOT_END();
         }
-        lds_barrier();
-        if (kt + 2 < nk) issue(kt + 2, st);
+        mm(15, db, wb);
+#pragma unroll
+        for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
+        SLOT_END();
     }
+    wait_vmcnt<0>();
 
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        const int gn = n0 + ncol[nb];
+        const int gn = n0 + ncol0 + 32 * nb;
         if (gn >= C) continue;
 #pragma unroll
         for (int mb = 0; mb < 8; ++mb) {
@@ -233,9 +331,23 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
-    hipLaunchKernelGGL((dx_kernel<RK, false>), grid, block, 0, st, (const uint16_t*)a.dY, (const uint16_t*)a.W,
-                       a.Mt, (const uint16_t*)a.B, (const uint16_t*)a.A, (uint16_t*)a.dX, a.L, (int)a.R,
-                       (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    // fixed-offset copies: whole tiles and K-steps, and per-lane byte
+    // offsets (256 dY rows of R, 64 W rows of C, 256 M^T rows) inside 32 bits
+    const int64_t wprT = (a.R + 31) / 32;
+    const bool ragged = a.L % BM != 0 || a.C % BN != 0 || a.R % BK != 0 ||
+                        (int64_t)BM * a.R * 2 >= (1ll << 31) || (int64_t)BK * a.C * 2 >= (1ll << 31) ||
+                        (int64_t)BN * wprT * 4 >= (1ll << 31);
+    auto* dY = (const uint16_t*)a.dY;
+    auto* W = (const uint16_t*)a.W;
+    auto* B = (const uint16_t*)a.B;
+    auto* A = (const uint16_t*)a.A;
+    auto* dX = (uint16_t*)a.dX;
+    if (ragged)
+        hipLaunchKernelGGL((dx_kernel<RK, true>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
+                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    else
+        hipLaunchKernelGGL((dx_kernel<RK, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
+                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
 }
 
