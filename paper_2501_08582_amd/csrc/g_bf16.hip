@@ -39,10 +39,14 @@ constexpr int GT_BYTES = BN * GT_PITCH;            // 128 KiB
 constexpr int EP_MT = 0;                           // M^T words [j][8]: 8 KiB
 constexpr int EP_LUT = 8192;                       // select LUT: 4 KiB
 constexpr int EP_B = 12288;                        // B block [i][32*JB] bf16: up to 64 KiB
+constexpr int EP_X = 12288 + BM * 64 * 4;           // dA exchange [2][16][64] fp32: 8 KiB (after the largest B block)
 constexpr int EP_A = SMEM;                         // A block [32 j'][256 j]: 16 KiB
 constexpr int SMEM_ALL = SMEM + 32 * kRowBytes;
 
-template <int RK>
+// RAGGED: some tile reaches past R, C or the token count L (copies check
+// every lane and read the zero page outside the tensors); otherwise copies
+// use uniform bases plus fixed per-lane offsets.
+template <int RK, bool RAGGED>
 __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
@@ -50,7 +54,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n) {
     constexpr int JB = (RK + 1) / 2;  // 32-wide blocks of the rank
     static_assert(GT_BYTES <= SMEM, "G^T tile fits");
-    static_assert(EP_B + BM * 32 * JB * 2 <= SMEM, "B block fits");
+    static_assert(EP_B + BM * 32 * JB * 2 <= EP_X && EP_X + 2 * 16 * kWave * 4 <= SMEM, "B block and dA exchange fit");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM_ALL];
 
     const int tid = threadIdx.x;
@@ -74,15 +78,31 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const int pchunk = lane & 31;
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
-    auto copy_pair = [&](int q, int64_t k0, uint32_t sb) {
+    uint32_t offD[LOADS], offX[LOADS];
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
         const int row = 2 * (LOADS * wave + q) + h;
         const int lc = swz_chunk(row, pchunk);
-        const int64_t gl = k0 + row;
-        const int gi = i0 + lc * 8, gj = j0 + lc * 8;
-        const void* a = (gl < L && gi < R) ? (const void*)(dY + gl * R + gi) : (const void*)zsrc;
-        const void* b = (gl < L && gj < C) ? (const void*)(X + gl * C + gj) : (const void*)zsrc;
-        copy16_to_lds(a, sb + (LOADS * wave + q) * 1024);
-        copy16_to_lds(b, sb + TILEB + (LOADS * wave + q) * 1024);
+        offD[q] = (uint32_t)((row * R + lc * 8) * 2);
+        offX[q] = (uint32_t)((row * C + lc * 8) * 2);
+    }
+    const uint16_t* dYt = uniform_ptr(dY + i0);
+    const uint16_t* Xt = uniform_ptr(X + j0);
+    auto copy_pair = [&](int q, int64_t k0, uint32_t sb) {
+        const uint32_t da = sb + (LOADS * wave + q) * 1024, xa = da + TILEB;
+        if constexpr (!RAGGED) {
+            copy16s_to_lds(uniform_ptr(dYt + k0 * R), offD[q], da);
+            copy16s_to_lds(uniform_ptr(Xt + k0 * C), offX[q], xa);
+        } else {
+            const int row = 2 * (LOADS * wave + q) + h;
+            const int lc = swz_chunk(row, pchunk);
+            const int64_t gl = k0 + row;
+            const int gi = i0 + lc * 8, gj = j0 + lc * 8;
+            const void* a = (gl < L && gi < R) ? (const void*)(dY + gl * R + gi) : (const void*)zsrc;
+            const void* b = (gl < L && gj < C) ? (const void*)(X + gl * C + gj) : (const void*)zsrc;
+            copy16_to_lds(a, da);
+            copy16_to_lds(b, xa);
+        }
     };
 
     // Per-lane fragment offsets inside a stage (sub-step rows added later).
@@ -172,9 +192,11 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     }
     stage_barrier<0>();
 
-    // ---- epilogue 1: side data into the (now idle) stage buffers:
-    //   M^T words of the tile [j][8 words], the select LUT, and B[i0.., :]
-    //   as [i][32*JB] (rank padded with zeros).
+    // ---- epilogue 1: side data, all requests in flight together:
+    //   M^T words of the tile [j][8 words] and the A block of rank block 0
+    //   (copies into LDS), the select LUT, and B[i0 .. i0+255][0 .. 32*JB)
+    //   as [i][32*JB] with ranks >= r zero: thread t loads row i0 + t with
+    //   16-byte loads (all issued before the first use).
     uint32_t* mtl = (uint32_t*)(smem + EP_MT);
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -185,12 +207,40 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
         copy4_to_lds((gj < C && giw < wprT) ? (const void*)(Mt + (int64_t)gj * wprT + giw) : (const void*)zsrc,
                      lds0 + EP_MT + 256 * blk);
     }
+    auto copy_a_block = [&](int jb) {  // A[32jb .. +31][j0 .. j0+255] -> EP_A
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {          // 32 rows x 512 B = 16 copies, 4 per wave
+            const int blk = 4 * wave + q;
+            const int row = 2 * blk + h;
+            const int lc = swz_chunk(row, lane & 31);
+            const int jr = 32 * jb + row, gj = j0 + 8 * lc;
+            copy16_to_lds((jr < r && gj < C) ? (const void*)(Am + (int64_t)jr * C + gj) : (const void*)zsrc,
+                          lds0 + EP_A + 1024 * blk);
+        }
+    };
+    copy_a_block(0);
     *(u32x4*)(smem + EP_LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
-    uint16_t* btl = (uint16_t*)(smem + EP_B);
-    for (int e = tid; e < BM * 32 * JB; e += NT) {
-        const int il = e / (32 * JB), jr = e % (32 * JB);
-        const int gi = i0 + il;
-        btl[e] = (gi < R && jr < r) ? Bm[(int64_t)gi * r + jr] : (uint16_t)0;
+    {
+        const int gi = i0 + tid;
+        const bool b_vec = (r & 7) == 0;
+        u32x4 bv[4 * JB];
+#pragma unroll
+        for (int c = 0; c < 4 * JB; ++c) {
+            bv[c] = zero_u32x4();
+            const int jr0 = 8 * c;
+            if (gi < R && jr0 < r) {
+                const uint16_t* src = Bm + (int64_t)gi * r + jr0;
+                if (b_vec) {
+                    bv[c] = *(const u32x4*)src;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        bv[c][e >> 1] |= (jr0 + e < r ? (uint32_t)src[e] : 0u) << ((e & 1) * 16);
+                }
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 4 * JB; ++c) *(u32x4*)(smem + EP_B + 2 * (tid * 32 * JB + 8 * c)) = bv[c];
     }
     stage_barrier<0>();
 
@@ -217,11 +267,17 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     // ---- epilogue 3: dA[j'][j] += s * sum_i B[i][j'] G[i][j], with the masked
     // bf16 accumulators as the MFMA B operand (K = rows i in accumulator
     // order); the A operand B^T comes from the B block by transpose loads.
+    // The two waves with the same wj hold partial sums over the two halves of
+    // the tile's rows: for column blocks b = 0, 1 wave wi = 1 hands its partial
+    // to wave wi = 0 through LDS, for b = 2, 3 the other way round, so each dA
+    // element receives one atomic add per tile.
     {
         const int g = lane >> 4, jj = lane & 15;
+        float* xch = (float*)(smem + EP_X) + wj * 16 * kWave;  // [wj][v][lane]
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             const int gj = j0 + wj * 128 + 32 * b + l32;
+            const bool giver = (b < 2) == (wi == 1);
 #pragma unroll
             for (int jb = 0; jb < JB; ++jb) {
                 f32x16 da;
@@ -238,17 +294,26 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
                         da = mfma_32x32x16(frag_from_tr(lo, hi), as_bf16x8(gb[a][b][c]), da);
                     }
                 }
-                if (gj < C) {
+                if (giver) {
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
-                        if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
+                    for (int v = 0; v < 16; ++v) xch[v * kWave + lane] = da[v];
+                }
+                lds_barrier();
+                if (!giver) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) da[v] += xch[v * kWave + lane];
+                    if (gj < C) {
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
+                            if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
+                        }
                     }
                 }
+                lds_barrier();  // exchange slot free again
             }
         }
     }
-    lds_barrier();
 
     // ---- epilogue 4: G^T -> LDS as [j][i] (pitch 512 B; the quad of 16-byte
     // chunks is XORed with j % 8 so that transpose reads of 4 consecutive j
@@ -276,15 +341,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     // rank block at a time: A[32jb .. +31][j0 .. j0+255] is copied to LDS and
     // wave w accumulates rows i = 64w .. 64w+63 of the tile.
     for (int jb = 0; jb < JB; ++jb) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {          // 32 rows x 512 B = 16 copies, 4 per wave
-            const int blk = 4 * wave + q;
-            const int row = 2 * blk + h;
-            const int lc = swz_chunk(row, lane & 31);
-            const int jr = 32 * jb + row, gj = j0 + 8 * lc;
-            copy16_to_lds((jr < r && gj < C) ? (const void*)(Am + (int64_t)jr * C + gj) : (const void*)zsrc,
-                          lds0 + EP_A + 1024 * blk);
-        }
+        if (jb > 0) copy_a_block(jb);  // block 0 was requested with the side data
         stage_barrier<0>();  // A block landed; G^T complete
 #pragma unroll
         for (int ib = 0; ib < 2; ++ib) {
@@ -323,8 +380,16 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     auto* X = (const uint16_t*)a.X;
     auto* B = (const uint16_t*)a.B;
     auto* A = (const uint16_t*)a.A;
-    hipLaunchKernelGGL((g_kernel<RK>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
-                       (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    // fixed-offset copies: whole tiles and K-steps, per-lane byte offsets
+    // (64 token rows of R or C) inside 32 bits
+    const bool ragged = a.R % BM != 0 || a.C % BN != 0 || a.L % BK != 0 ||
+                        (int64_t)BK * a.R * 2 >= (1ll << 31) || (int64_t)BK * a.C * 2 >= (1ll << 31);
+    if (ragged)
+        hipLaunchKernelGGL((g_kernel<RK, true>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+    else
+        hipLaunchKernelGGL((g_kernel<RK, false>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
     return hipGetLastError();
 }
 
