@@ -63,6 +63,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     float s, int tiles_m, int tiles_n) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
+    static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
     static_assert(16 * RK * kRowBytes <= Lay::STAGE, "A block fits one stage");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
@@ -309,20 +310,25 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
         SLOT_END();
     }
+    // ---- epilogue: round to bf16, stage the wave's 256 x 64 block in LDS
+    // (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
-
+    lds_barrier();  // every wave's copies landed and every read of the stages done
+    uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int gn = n0 + ncol0 + 32 * nb;
-        if (gn >= C) continue;
+    for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
+        for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t gm = m0 + 32 * mb + 8 * (v >> 2) + 4 * h + (v & 3);
-                if (gm < L) dX[gm * C + gn] = bf16_bits(acc[mb][nb][v]);
-            }
-        }
+            for (int v = 0; v < 16; ++v)
+                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v]);
+#pragma unroll 4
+    for (int it = 0; it < BM / 8; ++it) {
+        const int row = 8 * it + (lane >> 3), ch = lane & 7;
+        const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
+        const int64_t gm = m0 + row;
+        const int gn = n0 + 64 * wave + 8 * ch;
+        if (gm < L && gn < C) *(u32x4*)(dX + gm * C + gn) = v;
     }
 }
 

@@ -70,6 +70,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     int tiles_n) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
+    static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -324,22 +325,28 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
         SLOT_END();
     }
+    // ---- epilogue: (+bias), round to bf16, stage the wave's 256 x 64 block in
+    // LDS (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
-
-    // ---- epilogue: (+bias), round to bf16, store
+    lds_barrier();  // every wave's copies landed and every read of the stages done
+    uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
         const int gn = n0 + nrow0 + 32 * nb;
-        if (gn >= R) continue;
-        const float bv = bias ? bf16_bits_to_f32(bias[gn]) : 0.f;
+        const float bv = (bias != nullptr && gn < R) ? bf16_bits_to_f32(bias[gn]) : 0.f;
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
+        for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t gm = m0 + 32 * mb + 8 * (v >> 2) + 4 * h + (v & 3);
-                if (gm < L) Y[gm * R + gn] = bf16_bits(acc[mb][nb][v] + bv);
-            }
-        }
+            for (int v = 0; v < 16; ++v)
+                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v] + bv);
+    }
+#pragma unroll 4
+    for (int it = 0; it < BM / 8; ++it) {
+        const int row = 8 * it + (lane >> 3), ch = lane & 7;
+        const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
+        const int64_t gm = m0 + row;
+        const int gn = n0 + 64 * wave + 8 * ch;
+        if (gm < L && gn < R) *(u32x4*)(Y + gm * R + gn) = v;
     }
 }
 
