@@ -43,12 +43,6 @@ def parse():
     return ap.parse_args()
 
 
-def to_dev(a, dtype, torch, np):
-    if dtype == "bf16":
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
-    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
-
-
 def cpu_baseline(inp, args):
     """The fp64 oracle on the same workload, timed on the host cores."""
     import numpy as np
@@ -95,51 +89,22 @@ def main():
               "(the layer shards by tokens, see the design notes)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
-    from paper_2501_08582_amd import _lib, costs, ops, synth
+    from paper_2501_08582_amd import costs, synth
+    from paper_2501_08582_amd.step import LayerStep
 
     wl = synth.workload(args.workload)
     inp = synth.make(wl)
     dt = wl.dtype
     R, C, L, r, s = wl.R, wl.C, wl.L, wl.r, wl.scale
-    fmt = ops.TWO_FOUR if wl.mask == "2:4" else ops.BITMAP
     torch.cuda.set_device(0)
-
-    X, W, B, A, dY = (to_dev(t, dt, torch, np) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
-    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
-    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
-    Y = torch.empty((L, R), dtype=tdt, device="cuda")
-    dX = torch.empty((L, C), dtype=tdt, device="cuda")
-    dB = torch.empty((R, r), dtype=torch.float32, device="cuda")
-    dA = torch.empty((r, C), dtype=torch.float32, device="cuda")
-    p = _lib.problem(R, C, L, r, s, _lib.DTYPE_BF16 if dt == "bf16" else _lib.DTYPE_F32,
-                     _lib.MASK_2_4 if fmt == ops.TWO_FOUR else _lib.MASK_BITMAP)
-    p_reuse = _lib.problem(R, C, L, r, s, p.dtype, p.mask_format, _lib.FLAG_REUSE_MASK_T)
-    ws = _lib.workspace_bytes(p)
-    wsbuf = torch.empty(max(ws, 1), dtype=torch.uint8, device="cuda")
+    layer = LayerStep(inp)
+    ws = layer.ws
     stream = torch.cuda.current_stream()
-    sh = stream.cuda_stream
-    ptr = lambda t: t.data_ptr()  # noqa: E731
 
     def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        _lib.check(_lib.forward(p, ptr(X), ptr(W), ptr(M), ptr(B), ptr(A), None, ptr(Y), None, 0, sh),
-                   "lors_forward")
-        if ev is not None:
-            ev[1].record(stream)
-        # the data half rebuilds the transposed mask in the workspace; the
-        # weight half of the same step reuses it
-        _lib.check(_lib.backward_data(p, ptr(dY), ptr(W), ptr(M), ptr(B), ptr(A), ptr(dX), ptr(wsbuf), ws,
-                                      sh), "lors_backward_data")
-        if ev is not None:
-            ev[2].record(stream)
-        _lib.check(_lib.backward_weight(p_reuse, ptr(dY), ptr(X), ptr(M), ptr(B), ptr(A), ptr(dB), ptr(dA),
-                                        None, ptr(wsbuf), ws, sh), "lors_backward_weight")
-        if ev is not None:
-            ev[3].record(stream)
+        layer.run(ev)
 
     for _ in range(args.warmup):
         step()

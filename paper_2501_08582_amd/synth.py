@@ -134,10 +134,17 @@ def workload(name: str) -> Workload:
 # ---------------------------------------------------------------------------
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round finite float32 values to bf16 (RNE) and return the uint16 patterns."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    return ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    """Round finite float32 values to bf16 (RNE) and return the uint16 patterns.
+
+    For finite inputs the bit pattern is at most 0xFF7FFFFF, so adding the
+    rounding increment (at most 0x8000) cannot overflow 32 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
 
 
 def _bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
