@@ -40,7 +40,45 @@ def parse():
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host time spent on the oracle sample")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="short program for hardware-counter runs: one step, a device copy of "
+                         "COPY_BYTES (the calibration of the byte counters), one more step")
     return ap.parse_args()
+
+
+COPY_BYTES = 256 << 20
+
+# Sources that define each timed kernel: a traffic figure measured with
+# hardware counters is reported only while these files are unchanged.
+KERNEL_SOURCES = {
+    "fwd_kernel": ["fwd_bf16.hip"],
+    "dx_kernel": ["dx_bf16.hip"],
+    "g_kernel": ["g_bf16.hip"],
+}
+COMMON_SOURCES = ["gemm_common.hpp", "device_common.hpp", "kernels.hpp"]
+
+
+def kernel_digest(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
+        with open(os.path.join(ROOT, "paper_2501_08582_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from profiles/traffic_<workload>.txt
+    (rocprofv3 FETCH_SIZE / WRITE_SIZE, calibrated on a copy of known size),
+    or None when absent or taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) == 5 and f[0] == kernel:
+            return int(f[3]) if f[4] == kernel_digest(kernel) else None
+    return None
 
 
 def cpu_baseline(inp, args):
@@ -103,24 +141,35 @@ def main():
     ws = layer.ws
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
-        layer.run(ev)
+    def step():
+        layer.run()
+
+    if args.pmc_probe:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        step()
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        step()
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_probe": True, "workload": wl.name, "copy_bytes": COPY_BYTES}), flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # Timed region: K steps bracketed by a device synchronisation on both
-    # sides; per-kernel events on the launch stream inside it.
+    # sides, HIP events on the launch stream at its two ends only.
     torch.cuda.reset_peak_memory_stats()
     mem0 = torch.cuda.memory_allocated()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
-    for k in range(args.steps):
-        step(evs[k])
+    for _ in range(args.steps):
+        step()
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -128,18 +177,30 @@ def main():
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
 
-    per = {"fwd": [], "bwd_data": [], "bwd_weight": []}
-    for e in evs:
-        per["fwd"].append(e[0].elapsed_time(e[1]))
-        per["bwd_data"].append(e[1].elapsed_time(e[2]))
-        per["bwd_weight"].append(e[2].elapsed_time(e[3]))
-    avg = {k: sum(v) / len(v) for k, v in per.items()}
+    # Per-kernel durations: each call issued K times back to back on the same
+    # stream between two events (the data half with the transposed mask
+    # already built, i.e. the dX kernel alone; the weight half is the dA/dB
+    # clear plus the G kernel).
+    def per_call(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps
+
+    avg = {"fwd": per_call(layer.forward),
+           "bwd_data": per_call(lambda: layer.backward_data(reuse_mask_t=True)),
+           "bwd_weight": per_call(layer.backward_weight)}
     kflops = {"fwd": costs.fwd_flops(R, C, L, r), "bwd_data": costs.dx_flops(R, C, L, r),
               "bwd_weight": costs.g_flops(R, C, L, r)}
     kbytes = costs.min_hbm_bytes(R, C, L, r, elt=2 if dt == "bf16" else 4)
     kbytes = {"fwd": kbytes["fwd"], "bwd_data": kbytes["dx"], "bwd_weight": kbytes["g"]}
-    kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel (+ mask transpose)",
+    kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel",
                     "bwd_weight": "g_kernel (+ dA/dB clear)"}
+    kernel_ids = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel", "bwd_weight": "g_kernel"}
 
     flops = costs.algorithmic_flops(R, C, L, r)
     value = flops / (ms_step * 1e-3) / 1e12
@@ -180,7 +241,7 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": measured_traffic(wl.name, kernel_ids[dom]),
             "algorithmic_bytes": kbytes[dom],
         },
         "wall_s_timed": round(wall, 4),

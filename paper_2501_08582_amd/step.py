@@ -9,8 +9,6 @@ allocates buffers and passes pointers.
 """
 from __future__ import annotations
 
-from typing import Optional, Sequence
-
 import numpy as np
 import torch
 
@@ -50,24 +48,33 @@ class LayerStep:
         self.ws = _lib.workspace_bytes(self.p)
         self.wsbuf = torch.empty(max(self.ws, 1), dtype=torch.uint8, device="cuda")
 
-    def run(self, events: Optional[Sequence[torch.cuda.Event]] = None) -> None:
-        """One pass.  ``events`` (4 of them) are recorded before the forward,
-        between the calls, and after the weight gradient."""
+    def _ptrs(self):
         st = torch.cuda.current_stream()
-        sh = st.cuda_stream
-        ptr = lambda t: t.data_ptr()  # noqa: E731
-        if events is not None:
-            events[0].record(st)
-        _lib.check(_lib.forward(self.p, ptr(self.X), ptr(self.W), ptr(self.M), ptr(self.B), ptr(self.A), None,
-                                ptr(self.Y), None, 0, sh), "lors_forward")
-        if events is not None:
-            events[1].record(st)
-        _lib.check(_lib.backward_data(self.p, ptr(self.dY), ptr(self.W), ptr(self.M), ptr(self.B), ptr(self.A),
-                                      ptr(self.dX), ptr(self.wsbuf), self.ws, sh), "lors_backward_data")
-        if events is not None:
-            events[2].record(st)
-        _lib.check(_lib.backward_weight(self.p_reuse, ptr(self.dY), ptr(self.X), ptr(self.M), ptr(self.B),
-                                        ptr(self.A), ptr(self.dB), ptr(self.dA), None, ptr(self.wsbuf), self.ws, sh),
-                   "lors_backward_weight")
-        if events is not None:
-            events[3].record(st)
+        return st, st.cuda_stream
+
+    def forward(self) -> None:
+        _, sh = self._ptrs()
+        _lib.check(_lib.forward(self.p, self.X.data_ptr(), self.W.data_ptr(), self.M.data_ptr(), self.B.data_ptr(),
+                                self.A.data_ptr(), None, self.Y.data_ptr(), None, 0, sh), "lors_forward")
+
+    def backward_data(self, reuse_mask_t: bool = False) -> None:
+        """dX; builds the transposed mask in the workspace unless told it is
+        already there (then only the dX kernel runs)."""
+        _, sh = self._ptrs()
+        p = self.p_reuse if reuse_mask_t else self.p
+        _lib.check(_lib.backward_data(p, self.dY.data_ptr(), self.W.data_ptr(), self.M.data_ptr(), self.B.data_ptr(),
+                                      self.A.data_ptr(), self.dX.data_ptr(), self.wsbuf.data_ptr(), self.ws, sh),
+                   "lors_backward_data")
+
+    def backward_weight(self) -> None:
+        """dB, dA, reusing the transposed mask built by backward_data."""
+        _, sh = self._ptrs()
+        _lib.check(_lib.backward_weight(self.p_reuse, self.dY.data_ptr(), self.X.data_ptr(), self.M.data_ptr(),
+                                        self.B.data_ptr(), self.A.data_ptr(), self.dB.data_ptr(), self.dA.data_ptr(),
+                                        None, self.wsbuf.data_ptr(), self.ws, sh), "lors_backward_weight")
+
+    def run(self) -> None:
+        """One pass: forward, data backward, weight backward."""
+        self.forward()
+        self.backward_data()
+        self.backward_weight()
