@@ -40,6 +40,9 @@ def parse():
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host time spent on the oracle sample")
+    ap.add_argument("--ste", action="store_true",
+                    help="straight-through adapter gradients (Section 2.3) in the weight half; "
+                         "flops counted are those of that method")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="short program for hardware-counter runs: one step, a device copy of "
                          "COPY_BYTES (the calibration of the byte counters), one more step")
@@ -72,7 +75,7 @@ def measured_traffic(workload: str, kernel: str):
     (rocprofv3 FETCH_SIZE / WRITE_SIZE, calibrated on a copy of known size),
     or None when absent or taken on different kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
-    if not os.path.exists(path):
+    if kernel is None or not os.path.exists(path):
         return None
     for line in open(path):
         f = line.split()
@@ -137,7 +140,7 @@ def main():
     dt = wl.dtype
     R, C, L, r, s = wl.R, wl.C, wl.L, wl.r, wl.scale
     torch.cuda.set_device(0)
-    layer = LayerStep(inp)
+    layer = LayerStep(inp, ste=args.ste)
     ws = layer.ws
     stream = torch.cuda.current_stream()
 
@@ -195,14 +198,15 @@ def main():
            "bwd_data": per_call(lambda: layer.backward_data(reuse_mask_t=True)),
            "bwd_weight": per_call(layer.backward_weight)}
     kflops = {"fwd": costs.fwd_flops(R, C, L, r), "bwd_data": costs.dx_flops(R, C, L, r),
-              "bwd_weight": costs.g_flops(R, C, L, r)}
+              "bwd_weight": costs.ste_weight_flops(R, C, L, r) if args.ste else costs.g_flops(R, C, L, r)}
     kbytes = costs.min_hbm_bytes(R, C, L, r, elt=2 if dt == "bf16" else 4)
     kbytes = {"fwd": kbytes["fwd"], "bwd_data": kbytes["dx"], "bwd_weight": kbytes["g"]}
     kernel_names = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel",
-                    "bwd_weight": "g_kernel (+ dA/dB clear)"}
-    kernel_ids = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel", "bwd_weight": "g_kernel"}
+                    "bwd_weight": ("straight-through kernels (+ dA/dB clear)" if args.ste
+                                   else "g_kernel (+ dA/dB clear)")}
+    kernel_ids = {"fwd": "fwd_kernel", "bwd_data": "dx_kernel", "bwd_weight": None if args.ste else "g_kernel"}
 
-    flops = costs.algorithmic_flops(R, C, L, r)
+    flops = costs.ste_step_flops(R, C, L, r) if args.ste else costs.algorithmic_flops(R, C, L, r)
     value = flops / (ms_step * 1e-3) / 1e12
     peak = PEAK_TFLOPS[dt]
     dom = max(avg, key=avg.get)
@@ -222,7 +226,8 @@ def main():
         "dtype": dt,
         "data": "synthetic (seeded, Llama-shaped; random-init weights and adapters)",
         "config": {"workload": wl.name, "R": R, "C": C, "L": L, "r": r, "mask": wl.mask,
-                   "sparsity": wl.sparsity, "scale": s},
+                   "sparsity": wl.sparsity, "scale": s,
+                   "weight_gradient": "straight-through" if args.ste else "exact masked"},
         "pct_mfma_peak": round(100.0 * value / peak, 2),
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),

@@ -96,8 +96,14 @@ typedef enum lors_mask_format {
     LORS_MASK_2_4 = 1
 } lors_mask_format_t;
 
-/* Reserved: the straight-through, re-associated backward of Section 2.3
- * (Algorithm 2).  Currently rejected with LORS_ERR_UNSUPPORTED. */
+/* Backward calls: the straight-through, re-associated adapter gradients of
+ * Section 2.3 (Algorithm 2) instead of the exact masked ones.  The mask is
+ * dropped from the weight gradient, which then never forms:
+ *   P = X . A^T, Q = dY . B (L x r, bf16 in the workspace),
+ *   dB = s . dY^T . P, dA = s . Q^T . X.
+ * dX is unchanged (exact, with the recomputed masked weight).  bf16 only
+ * (fp32: LORS_ERR_UNSUPPORTED).  The workspace grows by the P, Q and B^T
+ * buffers (lors_workspace_bytes accounts for them). */
 #define LORS_FLAG_BWD_STE 0x1u
 
 /* Backward calls only: the workspace already holds the transposed mask that
@@ -123,7 +129,7 @@ typedef struct lors_problem {
     float scale;
     int32_t dtype;        /* lors_dtype_t */
     int32_t mask_format;  /* lors_mask_format_t */
-    uint32_t flags;       /* 0 or LORS_FLAG_REUSE_MASK_T */
+    uint32_t flags;       /* 0, LORS_FLAG_REUSE_MASK_T and/or LORS_FLAG_BWD_STE */
 } lors_problem_t;
 
 /* Human-readable name of a status code (static storage). */
@@ -174,7 +180,9 @@ lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C
 /* Device scratch bytes the backward calls (lors_backward, lors_backward_data,
  * lors_backward_weight) need for problem p: for bf16 the transposed bitmap of
  * the mask, 4 * C * ceil(R/32) bytes rounded up to 256 (about R*C/8, i.e.
- * 1/16 of W); 0 for fp32.  (size_t)-1 if p is invalid.  The workspace must be
+ * 1/16 of W), plus with LORS_FLAG_BWD_STE the P and Q buffers (2*L*r bytes
+ * each) and B^T (2*r*R bytes), each rounded up to 256; 0 for fp32.
+ * (size_t)-1 if p is invalid.  The workspace must be
  * 16-byte aligned, must not overlap any argument, and is overwritten; its
  * contents on return are unspecified.  lors_forward needs no workspace. */
 size_t lors_workspace_bytes(const lors_problem_t* p);

@@ -39,6 +39,8 @@ __all__ = [
     "dx_entries",
     "db_rows",
     "da_cols",
+    "ste_db_rows",
+    "ste_da_cols",
 ]
 
 
@@ -184,3 +186,19 @@ def da_cols(dY, X, M, B, s, cols) -> np.ndarray:
     (dY, B) = _f64(dY, B)
     G = np.where(_mask(M[:, cols]), dY.T @ Xc, 0.0)       # R x |cols|
     return s * (B.T @ G)
+
+
+def ste_db_rows(dY, X, A, s, rows) -> np.ndarray:
+    """Rows of the straight-through ``dB = s * dY^T @ (X @ A^T)`` (Section 2.3)."""
+    rows = np.asarray(rows)
+    dYr = np.asarray(dY[:, rows], dtype=np.float64)      # L x |rows|
+    (X, A) = _f64(X, A)
+    return s * (dYr.T @ (X @ A.T))
+
+
+def ste_da_cols(dY, X, B, s, cols) -> np.ndarray:
+    """Columns of the straight-through ``dA = s * (dY @ B)^T @ X`` (Section 2.3)."""
+    cols = np.asarray(cols)
+    Xc = np.asarray(X[:, cols], dtype=np.float64)        # L x |cols|
+    (dY, B) = _f64(dY, B)
+    return s * ((dY @ B).T @ Xc)

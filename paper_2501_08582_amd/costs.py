@@ -88,6 +88,17 @@ def algorithmic_flops(R, C, L, r) -> int:
     return fwd_flops(R, C, L, r) + dx_flops(R, C, L, r) + g_flops(R, C, L, r)
 
 
+def ste_weight_flops(R, C, L, r) -> int:
+    """Straight-through adapter gradients (Section 2.3): X.A^T, dY.B, dY^T.P,
+    Q^T.X -- 4Lr(R + C)."""
+    return 4 * L * r * (R + C)
+
+
+def ste_step_flops(R, C, L, r) -> int:
+    """Forward + dX + straight-through adapter gradients."""
+    return fwd_flops(R, C, L, r) + dx_flops(R, C, L, r) + ste_weight_flops(R, C, L, r)
+
+
 def executed_flops(R, C, L, r, fwd_tile_l: int, dx_tile_l: int) -> int:
     """Flops the fused kernels execute when every token tile re-merges W'."""
     fwd_merges = max(1, -(-L // fwd_tile_l)) if L else 0

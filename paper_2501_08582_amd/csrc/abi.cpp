@@ -50,7 +50,9 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
     if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
     if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
-    if ((p->flags & ~LORS_FLAG_REUSE_MASK_T) != 0u) return LORS_ERR_UNSUPPORTED;
+    if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE)) != 0u) return LORS_ERR_UNSUPPORTED;
+    // the straight-through backward exists for bf16 only
+    if ((p->flags & LORS_FLAG_BWD_STE) != 0u && p->dtype != LORS_DTYPE_BF16) return LORS_ERR_UNSUPPORTED;
     const int64_t row_align = p->dtype == LORS_DTYPE_BF16 ? 8 : 4;
     if (p->R % row_align != 0 || p->C % row_align != 0) return LORS_ERR_UNSUPPORTED;
     if (p->dtype == LORS_DTYPE_F32) {
@@ -97,11 +99,18 @@ size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
 
 // bf16 backward: the transposed bitmap M^T (C rows of ceil(R/32) words),
 // rounded up to 256 bytes.  The forward and the fp32 path need nothing.
+// bf16 workspace: the transposed mask bitmap, then (straight-through flag)
+// the P, Q and B^T buffers of the re-associated adapter gradients.
+static size_t mt_bytes(const lors_problem_t* p) {
+    const int64_t bytes = p->C * ((p->R + 31) / 32) * 4;
+    return static_cast<size_t>((bytes + 255) / 256 * 256);
+}
 size_t lors_workspace_bytes(const lors_problem_t* p) {
     if (p == nullptr || check_problem(p) != LORS_OK) return static_cast<size_t>(-1);
     if (p->dtype != LORS_DTYPE_BF16) return 0;
-    const int64_t bytes = p->C * ((p->R + 31) / 32) * 4;
-    return static_cast<size_t>((bytes + 255) / 256 * 256);
+    size_t n = mt_bytes(p);
+    if ((p->flags & LORS_FLAG_BWD_STE) != 0u) n += lors::ste_workspace_bytes(p->R, p->L, p->r);
+    return n;
 }
 
 // ---------------------------------------------------------------------------
@@ -299,6 +308,8 @@ lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* 
     a.dX = dX; a.dB = dB; a.dA = dA; a.dbias = dbias;
     a.Mt = (p->dtype == LORS_DTYPE_BF16) ? static_cast<const uint32_t*>(workspace) : nullptr;
     a.reuse_mt = (p->flags & LORS_FLAG_REUSE_MASK_T) != 0u;
+    a.ste = (p->flags & LORS_FLAG_BWD_STE) != 0u;
+    a.ste_ws = (a.ste && workspace) ? static_cast<uint8_t*>(workspace) + mt_bytes(p) : nullptr;
     return a;
 }
 
@@ -311,7 +322,8 @@ hipError_t build_mt(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
 
 hipError_t run_weight(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
     hipError_t e = lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
-    if (e == hipSuccess) e = bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
+    if (e == hipSuccess)
+        e = a.ste ? lors::launch_ste_bf16(a, s) : bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
     if (e == hipSuccess) e = bf16 ? lors::launch_dbias_bf16(a, s) : lors::launch_dbias_f32(a, s);
     return e;
 }
@@ -370,7 +382,8 @@ lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY, cons
     const lors::LayerArgs a = layer_args(p, dY, X, nullptr, M_packed, B, A, nullptr, dB, dA, dbias, workspace);
     const bool bf16 = p->dtype == LORS_DTYPE_BF16;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = build_mt(a, bf16, s);
+    // the straight-through adapter gradients do not read the mask
+    hipError_t e = a.ste ? hipSuccess : build_mt(a, bf16, s);
     if (e == hipSuccess) e = run_weight(a, bf16, s);
     return from_hip(e);
 }

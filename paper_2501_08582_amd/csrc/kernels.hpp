@@ -25,6 +25,8 @@ struct LayerArgs {
     float* dB;              // R x r
     float* dA;              // r x C
     float* dbias;           // R or nullptr
+    bool ste;               // straight-through adapter gradients (Section 2.3)
+    void* ste_ws;           // P, Q, B^T scratch of the straight-through path
 };
 
 // bf16 path
@@ -33,6 +35,8 @@ hipError_t launch_fwd_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_dx_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);
+hipError_t launch_ste_bf16(const LayerArgs& a, hipStream_t s);  // dB, dA of the straight-through backward
+size_t ste_workspace_bytes(int64_t R, int64_t L, int64_t r);
 hipError_t launch_dbias_bf16(const LayerArgs& a, hipStream_t s);
 
 // fp32 path

@@ -111,10 +111,10 @@ def mask_unpack(packed: torch.Tensor, R: int, C: int, mask_format=BITMAP) -> tor
     return dense
 
 
-def _problem(X2, W, B, mask_format, scale, L=None):
+def _problem(X2, W, B, mask_format, scale, L=None, flags=0):
     R, C = W.shape
     r = B.shape[1]
-    return _lib.problem(R, C, X2.shape[0] if L is None else L, r, scale, _dt(W), _fmt(mask_format))
+    return _lib.problem(R, C, X2.shape[0] if L is None else L, r, scale, _dt(W), _fmt(mask_format), flags)
 
 
 def forward(X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor, A: torch.Tensor,
@@ -134,10 +134,11 @@ def forward(X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor, 
     return out.view(*lead, R)
 
 
-def workspace_bytes(W: torch.Tensor, B: torch.Tensor, L: int, mask_format=BITMAP) -> int:
-    """Scratch bytes the backward needs (the transposed mask bitmap for bf16)."""
+def workspace_bytes(W: torch.Tensor, B: torch.Tensor, L: int, mask_format=BITMAP, ste: bool = False) -> int:
+    """Scratch bytes the backward needs (the transposed mask bitmap for bf16,
+    plus the P/Q/B^T buffers of the straight-through gradients)."""
     R, C = W.shape
-    p = _lib.problem(R, C, L, B.shape[1], 1.0, _dt(W), _fmt(mask_format))
+    p = _lib.problem(R, C, L, B.shape[1], 1.0, _dt(W), _fmt(mask_format), _lib.FLAG_BWD_STE if ste else 0)
     n = _lib.workspace_bytes(p)
     if n == 2**64 - 1:
         raise ValueError("invalid problem")
@@ -147,11 +148,14 @@ def workspace_bytes(W: torch.Tensor, B: torch.Tensor, L: int, mask_format=BITMAP
 def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor,
              A: torch.Tensor, scale: float, mask_format=BITMAP, need_dx: bool = True,
              need_dbias: bool = False, out: Optional[Tuple] = None,
-             workspace: Optional[torch.Tensor] = None):
-    """(dX, dB, dA, dbias) of the exact, masked gradient; dB/dA/dbias are fp32.
+             workspace: Optional[torch.Tensor] = None, ste: bool = False):
+    """(dX, dB, dA, dbias); dB/dA/dbias are fp32.
 
-    ``workspace`` (uint8, at least :func:`workspace_bytes`) is allocated here
-    when not given."""
+    By default dB, dA are the exact, masked gradient.  ``ste=True`` gives the
+    straight-through, re-associated adapter gradients of Section 2.3 (bf16
+    only); dX is the same either way.  ``workspace`` (uint8, at least
+    :func:`workspace_bytes` with the same ``ste``) is allocated here when not
+    given."""
     X2 = X.reshape(-1, X.shape[-1])
     dY2 = dY.reshape(-1, dY.shape[-1])
     dev = _dev(dY2, X2, W, M, B, A)
@@ -165,7 +169,7 @@ def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor
         dB = torch.empty((R, r), dtype=torch.float32, device=dev)
         dA = torch.empty((r, C), dtype=torch.float32, device=dev)
         dbias = torch.empty(R, dtype=torch.float32, device=dev) if need_dbias else None
-    p = _problem(X2, W, B, mask_format, scale)
+    p = _problem(X2, W, B, mask_format, scale, flags=_lib.FLAG_BWD_STE if ste else 0)
     need = _lib.workspace_bytes(p)
     if workspace is None and need:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
@@ -184,9 +188,10 @@ class LoRSLinearFn(torch.autograd.Function):
     and recomputes the merged weight in backward (weight recompute)."""
 
     @staticmethod
-    def forward(ctx, X, W, M, B, A, bias, scale, mask_format):
+    def forward(ctx, X, W, M, B, A, bias, scale, mask_format, ste=False):
         ctx.scale = float(scale)
         ctx.mask_format = mask_format
+        ctx.ste = bool(ste)
         ctx.has_bias = bias is not None
         ctx.save_for_backward(X, W, M, B, A)
         return forward(X, W, M, B, A, scale, mask_format, bias)
@@ -195,10 +200,12 @@ class LoRSLinearFn(torch.autograd.Function):
     def backward(ctx, dY):
         X, W, M, B, A = ctx.saved_tensors
         dX, dB, dA, dbias = backward(dY.contiguous(), X, W, M, B, A, ctx.scale, ctx.mask_format,
-                                     need_dx=ctx.needs_input_grad[0], need_dbias=ctx.has_bias)
+                                     need_dx=ctx.needs_input_grad[0], need_dbias=ctx.has_bias, ste=ctx.ste)
         return (dX, None, None, dB.to(B.dtype), dA.to(A.dtype),
-                dbias.to(W.dtype) if dbias is not None else None, None, None)
+                dbias.to(W.dtype) if dbias is not None else None, None, None, None)
 
 
-def lors_linear(X, W, M, B, A, scale, mask_format=BITMAP, bias=None):
-    return LoRSLinearFn.apply(X, W, M, B, A, bias, scale, mask_format)
+def lors_linear(X, W, M, B, A, scale, mask_format=BITMAP, bias=None, ste=False):
+    """Sparsity-preserved LoRA linear with autograd.  ``ste=True`` selects
+    the straight-through adapter gradients of Section 2.3."""
+    return LoRSLinearFn.apply(X, W, M, B, A, bias, scale, mask_format, ste)

@@ -26,9 +26,11 @@ def to_device(a: np.ndarray, dtype: str) -> torch.Tensor:
 
 
 class LayerStep:
-    """Device buffers of one layer plus its forward + backward pass."""
+    """Device buffers of one layer plus its forward + backward pass.
+    ``ste=True`` runs the straight-through adapter gradients (Section 2.3)
+    in the weight half instead of the exact masked ones."""
 
-    def __init__(self, inp: Inputs):
+    def __init__(self, inp: Inputs, ste: bool = False):
         wl = inp.wl
         self.wl = wl
         dt = wl.dtype
@@ -45,7 +47,8 @@ class LayerStep:
         lfmt = _lib.MASK_2_4 if self.fmt == ops.TWO_FOUR else _lib.MASK_BITMAP
         self.p = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt)
         self.p_reuse = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_REUSE_MASK_T)
-        self.ws = _lib.workspace_bytes(self.p)
+        self.p_weight = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_BWD_STE) if ste else self.p_reuse)
+        self.ws = max(_lib.workspace_bytes(self.p), _lib.workspace_bytes(self.p_weight))
         self.wsbuf = torch.empty(max(self.ws, 1), dtype=torch.uint8, device="cuda")
 
     def _ptrs(self):
@@ -69,7 +72,7 @@ class LayerStep:
     def backward_weight(self) -> None:
         """dB, dA, reusing the transposed mask built by backward_data."""
         _, sh = self._ptrs()
-        _lib.check(_lib.backward_weight(self.p_reuse, self.dY.data_ptr(), self.X.data_ptr(), self.M.data_ptr(),
+        _lib.check(_lib.backward_weight(self.p_weight, self.dY.data_ptr(), self.X.data_ptr(), self.M.data_ptr(),
                                         self.B.data_ptr(), self.A.data_ptr(), self.dB.data_ptr(), self.dA.data_ptr(),
                                         None, self.wsbuf.data_ptr(), self.ws, sh), "lors_backward_weight")
 

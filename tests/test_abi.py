@@ -178,7 +178,7 @@ def test_shape(lib, kw):
 
 
 @pytest.mark.parametrize("kw", [dict(R=60), dict(C=36), dict(dtype=_lib.DTYPE_F32, C=66),
-                                dict(flags=_lib.FLAG_BWD_STE)])
+                                dict(flags=0x4), dict(dtype=_lib.DTYPE_F32, flags=_lib.FLAG_BWD_STE)])
 def test_unsupported(lib, kw):
     assert _fwd(_p(**kw), _ptrs(6)) == _lib.ERR_UNSUPPORTED
 
@@ -212,6 +212,16 @@ def test_workspace_query(lib):
     assert _lib.workspace_bytes(_p(R=520, C=776)) == -(-776 * 17 * 4 // 256) * 256
     assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32)) == 0
     assert _lib.workspace_bytes(_p(R=0)) == 2**64 - 1
+
+
+def test_workspace_query_straight_through(lib):
+    # transposed mask, then P and Q (2*L*r bytes each) and B^T (2*r*R), each
+    # rounded up to 256 bytes
+    up = lambda n: -(-n // 256) * 256  # noqa: E731
+    for R, C, L, r in ((64, 64, 32, 8), (520, 776, 300, 5), (4096, 4096, 4096, 16), (4096, 14336, 8192, 64)):
+        mt = up(C * -(-R // 32) * 4)
+        want = mt + 2 * up(2 * L * r) + up(2 * r * R)
+        assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=_lib.FLAG_BWD_STE)) == want
 
 
 def test_workspace_errors(lib):

@@ -69,3 +69,28 @@ def test_full_size_sampled(name):
     print(name, (R, C, L, wl.r), errs, flush=True)
     for k, e in errs.items():
         assert e <= TOL["bf16"], f"{name} {k}: rel err {e:.3e}"
+
+
+@pytest.mark.parametrize("name", ["llama2_7b_q_proj", "llama3_8b_down_proj"])
+def test_full_size_straight_through_sampled(name):
+    """The straight-through weight half at full size: rows of dB and columns
+    of dA against the oracle's entry-wise evaluators."""
+    from paper_2501_08582_amd import ops
+    wl = synth.workload(name)
+    inp = synth.make(wl)
+    layer = LayerStep(inp)
+    ws = ops.workspace_bytes(layer.W, layer.B, wl.L, layer.fmt, ste=True)
+    wsbuf = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    dX, dB, dA, _ = ops.backward(layer.dY, layer.X, layer.W, layer.M, layer.B, layer.A, wl.scale, layer.fmt,
+                                 need_dx=False, workspace=wsbuf, ste=True)
+    torch.cuda.synchronize()
+    R, C, s = wl.R, wl.C, wl.scale
+    rng = np.random.default_rng(wl.seed + 7)
+    rows = _sample(rng, R, 3)
+    cols = _sample(rng, C, 3)
+    f = obf16.to_f64
+    X, A, B, dY = f(inp.X), f(inp.A), f(inp.B), f(inp.dY)
+    e_db = relerr(dB[torch.from_numpy(rows).cuda()].double().cpu().numpy(), olors.ste_db_rows(dY, X, A, s, rows))
+    e_da = relerr(dA[:, torch.from_numpy(cols).cuda()].double().cpu().numpy(), olors.ste_da_cols(dY, X, B, s, cols))
+    print(name, "straight-through", {"dB": e_db, "dA": e_da}, flush=True)
+    assert e_db <= TOL["bf16"] and e_da <= TOL["bf16"]

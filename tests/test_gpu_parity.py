@@ -309,3 +309,46 @@ def test_split_backward_with_mask_reuse(kind):
     # the reuse flag is accepted by the combined call too
     dX2, dB2, dA2, _ = ops.backward(dY, X, W, M, B, A, 2.0, fmt)
     assert torch.equal(dX2.view(torch.int16), dX0.view(torch.int16))
+
+
+# ---------------------------------------------------------------------------
+# straight-through, re-associated adapter gradients (Section 2.3)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name,R,C,L,r", [
+    ("llama2_7b_q_proj", 520, 776, 300, 16),        # ragged everywhere
+    ("llama2_7b_q_proj", 256, 256, 256, 64),
+    ("llama2_7b_q_proj", 264, 1032, 77, 5),         # odd rank
+    ("llama2_7b_q_proj", 512, 264, 260, 128),       # largest rank
+    ("llama2_7b_up_proj_2_4", 1024, 512, 700, 40),
+    ("llama2_7b_q_proj", 1032, 520, 1, 24),         # single token
+])
+def test_parity_straight_through(name, R, C, L, r):
+    inp = _inputs(name, R=R, C=C, L=L, r=r, seed=3 * R + L + r)
+    dt = inp.wl.dtype
+    X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    fmt = FMT[inp.wl.mask]
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
+    s = inp.wl.scale
+    dX, dB, dA, _ = ops.backward(dY, X, W, M, B, A, s, fmt, ste=True)
+    torch.cuda.synchronize()
+    f = lambda a: to_f64(a, dt)  # noqa: E731
+    rdX, rdB, rdA = olors.backward_ste(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), s)
+    errs = {"dX": relerr(dev_to_f64(dX), rdX), "dB": relerr(dev_to_f64(dB), rdB), "dA": relerr(dev_to_f64(dA), rdA)}
+    print(name, (R, C, L, r), "straight-through", errs, flush=True)
+    for k, e in errs.items():
+        assert e <= TOL[dt], f"{k}: rel err {e:.3e}"
+
+
+def test_straight_through_equals_exact_for_a_dense_mask():
+    """With M = 1 the straight-through gradient is the exact one: the two GPU
+    paths (re-associated products vs. the masked weight-gradient kernel) agree."""
+    inp = _inputs("llama2_7b_q_proj", R=512, C=768, L=384, r=32, seed=77)
+    dt = inp.wl.dtype
+    X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    M = ops.mask_pack(torch.ones(inp.wl.R, inp.wl.C, dtype=torch.uint8, device="cuda"), ops.BITMAP)
+    s = inp.wl.scale
+    _, dB_e, dA_e, _ = ops.backward(dY, X, W, M, B, A, s, ops.BITMAP)
+    _, dB_s, dA_s, _ = ops.backward(dY, X, W, M, B, A, s, ops.BITMAP, ste=True)
+    torch.cuda.synchronize()
+    assert relerr(dev_to_f64(dB_s), dev_to_f64(dB_e)) <= 1e-2
+    assert relerr(dev_to_f64(dA_s), dev_to_f64(dA_e)) <= 1e-2

@@ -356,3 +356,14 @@ def test_bf16_round_trip_against_torch():
     assert np.array_equal(bits, ref)
     back = obf16.to_f64(bits)
     assert np.array_equal(back, torch.from_numpy(ref.view(np.int16)).view(torch.bfloat16).double().numpy())
+
+
+def test_ste_entrywise_evaluators_match_full():
+    rng = np.random.default_rng(11)
+    R, C, L, r, s = 12, 16, 9, 3, 2.0
+    X, W, B, A, dY = (rng.standard_normal(sh) for sh in ((L, C), (R, C), (R, r), (r, C), (L, R)))
+    M = (rng.random((R, C)) < 0.5).astype(np.uint8)
+    _, dB, dA = lors.backward_ste(dY, X, W, M, B, A, s)
+    rows, cols = [0, 5, 11], [1, 15]
+    assert np.allclose(lors.ste_db_rows(dY, X, A, s, rows), dB[rows], rtol=1e-12, atol=1e-12)
+    assert np.allclose(lors.ste_da_cols(dY, X, B, s, cols), dA[:, cols], rtol=1e-12, atol=1e-12)

@@ -125,3 +125,13 @@ def test_known_totals():
     # 6RCL + 8rRC at the Llama-2-7B q_proj shape: 414.5 GFLOP
     assert abs(costs.algorithmic_flops(4096, 4096, 4096, 16) / 1e9 - 414.5) < 0.1
     assert abs(costs.algorithmic_flops(4096, 14336, 8192, 64) / 1e9 - 2916.3) < 0.1
+
+
+@pytest.mark.parametrize("dims", [(4096, 4096, 4096, 16), (11008, 4096, 2048, 64), (7, 13, 5, 3)])
+def test_ste_flops_match_paper_list(dims):
+    """The straight-through adapter gradients are the last four products of
+    the LoRS backward list (Algorithm 2), at 2 flops per MAC."""
+    R, C, L, r = dims
+    adapter = [op for op in costs.LORS_BWD if op[0] == "mm"][2:]
+    assert len(adapter) == 4
+    assert costs.ste_weight_flops(R, C, L, r) == 2 * costs.macs(adapter, R, C, L, r)
