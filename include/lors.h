@@ -180,8 +180,9 @@ lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C
 /* Device scratch bytes the backward calls (lors_backward, lors_backward_data,
  * lors_backward_weight) need for problem p: for bf16 the transposed bitmap of
  * the mask, 4 * C * ceil(R/32) bytes rounded up to 256 (about R*C/8, i.e.
- * 1/16 of W), plus with LORS_FLAG_BWD_STE the P and Q buffers (2*L*r bytes
- * each) and B^T (2*r*R bytes), each rounded up to 256; 0 for fp32.
+ * 1/16 of W), plus with LORS_FLAG_BWD_STE the P and Q buffers (2*L*rp
+ * bytes each, rp = r rounded up to a multiple of 32) and B^T (2*r*R bytes),
+ * each rounded up to 256; 0 for fp32.
  * (size_t)-1 if p is invalid.  The workspace must be
  * 16-byte aligned, must not overlap any argument, and is overwritten; its
  * contents on return are unspecified.  lors_forward needs no workspace. */

@@ -321,9 +321,9 @@ hipError_t build_mt(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
 }
 
 hipError_t run_weight(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
-    hipError_t e = lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
-    if (e == hipSuccess)
-        e = a.ste ? lors::launch_ste_bf16(a, s) : bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
+    // the straight-through launches clear dB and dA themselves
+    hipError_t e = a.ste ? lors::launch_ste_bf16(a, s) : lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
+    if (e == hipSuccess && !a.ste) e = bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
     if (e == hipSuccess) e = bf16 ? lors::launch_dbias_bf16(a, s) : lors::launch_dbias_f32(a, s);
     return e;
 }

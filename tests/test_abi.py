@@ -215,12 +215,14 @@ def test_workspace_query(lib):
 
 
 def test_workspace_query_straight_through(lib):
-    # transposed mask, then P and Q (2*L*r bytes each) and B^T (2*r*R), each
-    # rounded up to 256 bytes
+    # transposed mask, then P and Q (2*L*rp bytes each, rp = r rounded up to
+    # a multiple of 32) and B^T (2*r*R), each rounded up to 256 bytes
     up = lambda n: -(-n // 256) * 256  # noqa: E731
-    for R, C, L, r in ((64, 64, 32, 8), (520, 776, 300, 5), (4096, 4096, 4096, 16), (4096, 14336, 8192, 64)):
+    for R, C, L, r in ((64, 64, 32, 8), (520, 776, 300, 5), (4096, 4096, 4096, 16), (4096, 14336, 8192, 64),
+                       (512, 512, 77, 100)):
         mt = up(C * -(-R // 32) * 4)
-        want = mt + 2 * up(2 * L * r) + up(2 * r * R)
+        rp = -(-r // 32) * 32
+        want = mt + 2 * up(2 * L * rp) + up(2 * r * R)
         assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=_lib.FLAG_BWD_STE)) == want
 
 
