@@ -32,12 +32,25 @@ class LayerStep:
 
     def __init__(self, inp: Inputs, ste: bool = False):
         wl = inp.wl
+        dt = wl.dtype
+        tensors = [to_device(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY)]
+        self._setup(wl, *tensors, torch.from_numpy(inp.M).cuda(), ste)
+
+    @classmethod
+    def from_device(cls, wl, X, W, B, A, dY, M_dense, ste: bool = False) -> "LayerStep":
+        """Same, from device tensors of the workload's shapes and dtype
+        (M_dense: uint8 0/1, R x C)."""
+        self = cls.__new__(cls)
+        self._setup(wl, X, W, B, A, dY, M_dense, ste)
+        return self
+
+    def _setup(self, wl, X, W, B, A, dY, M_dense, ste):
         self.wl = wl
         dt = wl.dtype
         R, C, L, r = wl.R, wl.C, wl.L, wl.r
-        self.X, self.W, self.B, self.A, self.dY = (to_device(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+        self.X, self.W, self.B, self.A, self.dY = X, W, B, A, dY
         self.fmt = _FMT[wl.mask]
-        self.M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), self.fmt)
+        self.M = ops.mask_pack(M_dense, self.fmt)
         tdt = torch.bfloat16 if dt == "bf16" else torch.float32
         self.Y = torch.empty((L, R), dtype=tdt, device="cuda")
         self.dX = torch.empty((L, C), dtype=tdt, device="cuda")
