@@ -21,7 +21,10 @@ Readings of the paper taken here (each is pinned by a CPU test):
 * masking is a select, so a masked entry is +0 whatever the other operand
   holds (the paper: the mask "zeros out" entries, Section 2.1);
 * the exact gradient keeps the mask on the weight gradient (SP-LoRA backward,
-  Section 2.2); the straight-through form of Section 2.3 drops it.
+  Section 2.2); the straight-through form of Section 2.3 drops it;
+* the gradient-based initialisation of Section 2.4 takes the singular vectors
+  of that masked weight gradient (its derivation sets the mask aside; the
+  masked G is the update a sparsity-preserving full fine-tune would apply).
 """
 from __future__ import annotations
 
@@ -41,6 +44,9 @@ __all__ = [
     "da_cols",
     "ste_db_rows",
     "ste_da_cols",
+    "gradient_init",
+    "init_objective",
+    "canonical_rows",
 ]
 
 
@@ -202,3 +208,45 @@ def ste_da_cols(dY, X, B, s, cols) -> np.ndarray:
     Xc = np.asarray(X[:, cols], dtype=np.float64)        # L x |cols|
     (dY, B) = _f64(dY, B)
     return s * ((dY @ B).T @ Xc)
+
+
+# ---------------------------------------------------------------------------
+# Gradient-based initialisation (Section 2.4)
+# ---------------------------------------------------------------------------
+
+def canonical_rows(V) -> np.ndarray:
+    """Each row multiplied by +-1 so that its entry of largest magnitude (the
+    first one on ties) is positive: singular vectors are only defined up to
+    sign."""
+    V = np.array(V, dtype=np.float64, copy=True)
+    if V.size == 0:
+        return V
+    idx = np.argmax(np.abs(V), axis=1)
+    sgn = np.sign(V[np.arange(V.shape[0]), idx])
+    sgn[sgn == 0] = 1.0
+    return V * sgn[:, None]
+
+
+def init_objective(G, A) -> float:
+    """The quantity the initialisation minimises, ``||G - G A^T A||_F``
+    (Section 2.4, in this repository's orientation: A is r x C)."""
+    G, A = _f64(G, A)
+    return float(np.linalg.norm(G - (G @ A.T) @ A))
+
+
+def gradient_init(dY, X, M, r: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Adapters ``(B0, A0)`` of the gradient-based initialisation.
+
+    Section 2.4: the R x r adapter starts at zero and the r x C adapter is
+    chosen so that the first update matches full fine-tuning as closely as a
+    rank-r product can, i.e. it minimises ``||G - G A^T A||`` over A with
+    orthonormal rows; the minimiser is the top r right singular vectors of G
+    (rows of A0), G being the first step's weight gradient (the masked G of
+    :func:`weight_gradient`).  Rows are in :func:`canonical_rows` form.
+    """
+    G = weight_gradient(dY, X, M)
+    R, C = G.shape
+    if r > min(R, C):
+        raise ValueError("rank above min(R, C)")
+    _, _, Vt = np.linalg.svd(G, full_matrices=False)
+    return np.zeros((R, r)), canonical_rows(Vt[:r])

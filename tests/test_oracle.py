@@ -367,3 +367,72 @@ def test_ste_entrywise_evaluators_match_full():
     rows, cols = [0, 5, 11], [1, 15]
     assert np.allclose(lors.ste_db_rows(dY, X, A, s, rows), dB[rows], rtol=1e-12, atol=1e-12)
     assert np.allclose(lors.ste_da_cols(dY, X, B, s, cols), dA[:, cols], rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Gradient-based initialisation (Section 2.4): pins that do not re-use the
+# oracle's own SVD call.
+# ---------------------------------------------------------------------------
+
+def _planted(R, C, r, gap, rng):
+    """G = U diag(sig) V^T with known orthonormal U (R x k), V (C x k)."""
+    k = min(R, C)
+    U, _ = np.linalg.qr(rng.standard_normal((R, k)))
+    V, _ = np.linalg.qr(rng.standard_normal((C, k)))
+    sig = np.concatenate([gap * np.arange(r, 0, -1, dtype=float) + gap, np.linspace(1.0, 0.1, k - r)])
+    return U, sig, V
+
+
+def test_gradient_init_recovers_planted_right_singular_vectors():
+    # With X = I (L = C) and dY = G^T, the weight gradient dY^T X is G itself,
+    # so the init must return the planted leading right singular vectors.
+    rng = np.random.default_rng(21)
+    R, C, r = 24, 16, 3
+    U, sig, V = _planted(R, C, r, 10.0, rng)
+    G = (U * sig) @ V.T
+    X = np.eye(C)
+    dY = G.T.copy()
+    M = np.ones((R, C), dtype=np.uint8)
+    B0, A0 = lors.gradient_init(dY, X, M, r)
+    assert B0.shape == (R, r) and not B0.any()
+    want = lors.canonical_rows(V[:, :r].T)
+    assert np.allclose(A0, want, atol=1e-10)
+
+
+def test_gradient_init_meets_the_eckart_young_bound():
+    # The minimised objective equals the energy of the trailing singular
+    # values of the planted matrix (Eckart-Young), and any other orthonormal
+    # r x C matrix does worse.
+    rng = np.random.default_rng(22)
+    R, C, r = 20, 30, 4
+    U, sig, V = _planted(R, C, r, 3.0, rng)
+    G = (U * sig) @ V.T
+    M = np.ones((R, C), dtype=np.uint8)
+    _, A0 = lors.gradient_init(G.T.copy(), np.eye(C), M, r)
+    best = np.sqrt(np.sum(sig[r:] ** 2))
+    assert abs(lors.init_objective(G, A0) - best) < 1e-10 * best
+    Q, _ = np.linalg.qr(rng.standard_normal((C, r)))
+    assert lors.init_objective(G, Q.T) > best * 1.01
+    assert np.allclose(A0 @ A0.T, np.eye(r), atol=1e-12)
+
+
+def test_gradient_init_uses_the_masked_gradient():
+    # The subspace must be that of the masked gradient, built here entry by
+    # entry with loops, not that of dY^T X: checked through the eigenvectors
+    # of G^T G.
+    rng = np.random.default_rng(23)
+    R, C, L, r = 6, 5, 7, 2
+    dY, X = rng.standard_normal((L, R)), rng.standard_normal((L, C))
+    M = (rng.random((R, C)) < 0.5).astype(np.uint8)
+    G = np.zeros((R, C))
+    for i in range(R):
+        for j in range(C):
+            if M[i, j]:
+                G[i, j] = sum(dY[l, i] * X[l, j] for l in range(L))
+    _, A0 = lors.gradient_init(dY, X, M, r)
+    # A0 spans the top-r right singular subspace of G: G^T G A0^T = A0^T diag(ev)
+    GtG = G.T @ G
+    proj = A0.T @ A0
+    assert np.allclose(GtG @ A0.T, proj @ GtG @ A0.T, atol=1e-10)
+    ev = np.sort(np.linalg.eigvalsh(GtG))[::-1]
+    assert np.isclose(np.trace(A0 @ GtG @ A0.T), ev[:r].sum(), rtol=1e-10)
