@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--ste", action="store_true",
                     help="straight-through adapter gradients (Section 2.3) in the weight half; "
                          "flops counted are those of that method")
+    ap.add_argument("--sparse-mfma", action="store_true",
+                    help="2:4 workloads: forward on the structured-sparse MFMA")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="short program for hardware-counter runs: one step, a device copy of "
                          "COPY_BYTES (the calibration of the byte counters), one more step")
@@ -140,7 +142,7 @@ def main():
     dt = wl.dtype
     R, C, L, r, s = wl.R, wl.C, wl.L, wl.r, wl.scale
     torch.cuda.set_device(0)
-    layer = LayerStep(inp, ste=args.ste)
+    layer = LayerStep(inp, ste=args.ste, sparse_mfma=args.sparse_mfma)
     ws = layer.ws
     stream = torch.cuda.current_stream()
 
@@ -227,7 +229,8 @@ def main():
         "data": "synthetic (seeded, Llama-shaped; random-init weights and adapters)",
         "config": {"workload": wl.name, "R": R, "C": C, "L": L, "r": r, "mask": wl.mask,
                    "sparsity": wl.sparsity, "scale": s,
-                   "weight_gradient": "straight-through" if args.ste else "exact masked"},
+                   "weight_gradient": "straight-through" if args.ste else "exact masked",
+                   "forward_mfma": "structured-sparse" if args.sparse_mfma else "dense"},
         "pct_mfma_peak": round(100.0 * value / peak, 2),
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),

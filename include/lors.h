@@ -114,6 +114,16 @@ typedef enum lors_mask_format {
  * lors_backward_weight of one step. */
 #define LORS_FLAG_REUSE_MASK_T 0x2u
 
+/* Forward only: with a 2:4 mask, multiply on gfx950's structured-sparse MFMA
+ * (the 2:4 pattern of Section 3.1): each merged W' tile is compressed in
+ * registers to its two kept values per group of 4, indexed by the packed
+ * mask codes, so the matrix cores do half the work of the dense product.
+ * Same result as the dense forward up to rounding order.  bf16, 2:4 masks
+ * and r <= 64 only (otherwise LORS_ERR_UNSUPPORTED).  Not the default: the
+ * fused forward is bound by its merge and operand traffic rather than by
+ * the matrix cores, so it is not faster today. */
+#define LORS_FLAG_FWD_SPARSE_MFMA 0x4u
+
 /*
  * Problem description.
  *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
@@ -129,7 +139,7 @@ typedef struct lors_problem {
     float scale;
     int32_t dtype;        /* lors_dtype_t */
     int32_t mask_format;  /* lors_mask_format_t */
-    uint32_t flags;       /* 0, LORS_FLAG_REUSE_MASK_T and/or LORS_FLAG_BWD_STE */
+    uint32_t flags;       /* 0 or LORS_FLAG_* bits (REUSE_MASK_T, BWD_STE, FWD_SPARSE_MFMA) */
 } lors_problem_t;
 
 /* Human-readable name of a status code (static storage). */

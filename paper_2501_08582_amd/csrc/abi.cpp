@@ -50,7 +50,12 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
     if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
     if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
-    if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE)) != 0u) return LORS_ERR_UNSUPPORTED;
+    if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE | LORS_FLAG_FWD_SPARSE_MFMA)) != 0u)
+        return LORS_ERR_UNSUPPORTED;
+    // the structured-sparse forward exists for bf16 2:4 masks up to rank 64
+    if ((p->flags & LORS_FLAG_FWD_SPARSE_MFMA) != 0u &&
+        (p->dtype != LORS_DTYPE_BF16 || p->mask_format != LORS_MASK_2_4 || p->r > 64))
+        return LORS_ERR_UNSUPPORTED;
     // the straight-through backward exists for bf16 only
     if ((p->flags & LORS_FLAG_BWD_STE) != 0u && p->dtype != LORS_DTYPE_BF16) return LORS_ERR_UNSUPPORTED;
     const int64_t row_align = p->dtype == LORS_DTYPE_BF16 ? 8 : 4;
@@ -260,6 +265,7 @@ lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W
     a.R = R; a.C = C; a.L = L; a.r = r;
     a.scale = p->scale;
     a.two_four = p->mask_format == LORS_MASK_2_4;
+    a.sparse_mfma = (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) != 0u;
     a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.bias = bias; a.Y = Y;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_fwd_bf16(a, s) : lors::launch_fwd_f32(a, s));

@@ -376,6 +376,7 @@ hipError_t launch_fmt(const LayerArgs& a, hipStream_t st) {
 
 template <int RK>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
+    if (a.two_four && a.sparse_mfma) return launch_fwd24_bf16(a, st);  // structured-sparse MFMA
     return a.two_four ? launch_fmt<RK, true>(a, st) : launch_fmt<RK, false>(a, st);
 }
 

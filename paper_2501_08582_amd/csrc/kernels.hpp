@@ -11,6 +11,7 @@ struct LayerArgs {
     int64_t R, C, L, r;
     float scale;
     bool two_four;          // packed mask layout: 2:4 codes (else bitmap)
+    bool sparse_mfma;       // forward on the structured-sparse MFMA (2:4, bf16, r <= 64)
     const void* X;          // L x C
     const void* W;          // R x C
     const uint32_t* M;      // R x ceil(C/32), the caller's layout
@@ -32,6 +33,7 @@ struct LayerArgs {
 // bf16 path
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_fwd_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
+hipError_t launch_fwd24_bf16(const LayerArgs& a, hipStream_t s);      // 2:4 mask, sparse MFMA, rank <= 64
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_dx_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);

@@ -119,15 +119,17 @@ def _problem(X2, W, B, mask_format, scale, L=None, flags=0):
 
 def forward(X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor, A: torch.Tensor,
             scale: float, mask_format=BITMAP, bias: Optional[torch.Tensor] = None,
-            out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Y = X . select(M, W + scale.B.A, 0)^T (+ bias).  X may have leading dims."""
+            out: Optional[torch.Tensor] = None, sparse_mfma: bool = False) -> torch.Tensor:
+    """Y = X . select(M, W + scale.B.A, 0)^T (+ bias).  X may have leading dims.
+    ``sparse_mfma`` (2:4 masks, bf16, r <= 64) multiplies on the structured-
+    sparse MFMA instead of the dense one."""
     lead = X.shape[:-1]
     X2 = X.reshape(-1, X.shape[-1])
     dev = _dev(X2, W, M, B, A, bias)
     R = W.shape[0]
     if out is None:
         out = torch.empty((X2.shape[0], R), dtype=W.dtype, device=dev)
-    p = _problem(X2, W, B, mask_format, scale)
+    p = _problem(X2, W, B, mask_format, scale, flags=_lib.FLAG_FWD_SPARSE_MFMA if sparse_mfma else 0)
     with torch.cuda.device(dev):
         _lib.check(_lib.forward(p, _ptr(X2), _ptr(W), _ptr(M), _ptr(B), _ptr(A), _ptr(bias), _ptr(out),
                                 None, 0, _stream(dev)), "lors_forward")

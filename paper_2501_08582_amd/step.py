@@ -28,23 +28,25 @@ def to_device(a: np.ndarray, dtype: str) -> torch.Tensor:
 class LayerStep:
     """Device buffers of one layer plus its forward + backward pass.
     ``ste=True`` runs the straight-through adapter gradients (Section 2.3)
-    in the weight half instead of the exact masked ones."""
+    in the weight half instead of the exact masked ones; ``sparse_mfma=True``
+    runs a 2:4 forward on the structured-sparse MFMA."""
 
-    def __init__(self, inp: Inputs, ste: bool = False):
+    def __init__(self, inp: Inputs, ste: bool = False, sparse_mfma: bool = False):
         wl = inp.wl
         dt = wl.dtype
         tensors = [to_device(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY)]
-        self._setup(wl, *tensors, torch.from_numpy(inp.M).cuda(), ste)
+        self._setup(wl, *tensors, torch.from_numpy(inp.M).cuda(), ste, sparse_mfma)
 
     @classmethod
-    def from_device(cls, wl, X, W, B, A, dY, M_dense, ste: bool = False) -> "LayerStep":
+    def from_device(cls, wl, X, W, B, A, dY, M_dense, ste: bool = False,
+                    sparse_mfma: bool = False) -> "LayerStep":
         """Same, from device tensors of the workload's shapes and dtype
         (M_dense: uint8 0/1, R x C)."""
         self = cls.__new__(cls)
-        self._setup(wl, X, W, B, A, dY, M_dense, ste)
+        self._setup(wl, X, W, B, A, dY, M_dense, ste, sparse_mfma)
         return self
 
-    def _setup(self, wl, X, W, B, A, dY, M_dense, ste):
+    def _setup(self, wl, X, W, B, A, dY, M_dense, ste, sparse_mfma=False):
         self.wl = wl
         dt = wl.dtype
         R, C, L, r = wl.R, wl.C, wl.L, wl.r
@@ -59,6 +61,8 @@ class LayerStep:
         ldt = _lib.DTYPE_BF16 if dt == "bf16" else _lib.DTYPE_F32
         lfmt = _lib.MASK_2_4 if self.fmt == ops.TWO_FOUR else _lib.MASK_BITMAP
         self.p = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt)
+        self.p_fwd = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_FWD_SPARSE_MFMA) if sparse_mfma
+                      else self.p)
         self.p_reuse = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_REUSE_MASK_T)
         self.p_weight = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_BWD_STE) if ste else self.p_reuse)
         self.ws = max(_lib.workspace_bytes(self.p), _lib.workspace_bytes(self.p_weight))
@@ -70,7 +74,7 @@ class LayerStep:
 
     def forward(self) -> None:
         _, sh = self._ptrs()
-        _lib.check(_lib.forward(self.p, self.X.data_ptr(), self.W.data_ptr(), self.M.data_ptr(), self.B.data_ptr(),
+        _lib.check(_lib.forward(self.p_fwd, self.X.data_ptr(), self.W.data_ptr(), self.M.data_ptr(), self.B.data_ptr(),
                                 self.A.data_ptr(), None, self.Y.data_ptr(), None, 0, sh), "lors_forward")
 
     def backward_data(self, reuse_mask_t: bool = False) -> None:

@@ -178,9 +178,20 @@ def test_shape(lib, kw):
 
 
 @pytest.mark.parametrize("kw", [dict(R=60), dict(C=36), dict(dtype=_lib.DTYPE_F32, C=66),
-                                dict(flags=0x4), dict(dtype=_lib.DTYPE_F32, flags=_lib.FLAG_BWD_STE)])
+                                dict(flags=0x8), dict(dtype=_lib.DTYPE_F32, flags=_lib.FLAG_BWD_STE),
+                                # the structured-sparse forward: bf16 2:4 masks up to rank 64 only
+                                dict(flags=_lib.FLAG_FWD_SPARSE_MFMA),
+                                dict(mask_format=_lib.MASK_2_4, dtype=_lib.DTYPE_F32, flags=_lib.FLAG_FWD_SPARSE_MFMA),
+                                dict(mask_format=_lib.MASK_2_4, r=65, flags=_lib.FLAG_FWD_SPARSE_MFMA)])
 def test_unsupported(lib, kw):
     assert _fwd(_p(**kw), _ptrs(6)) == _lib.ERR_UNSUPPORTED
+
+
+def test_sparse_mfma_flag_accepted_for_two_four(lib):
+    # validation only (a workspace query launches nothing)
+    for r in (1, 16, 64):
+        p = _p(mask_format=_lib.MASK_2_4, r=r, flags=_lib.FLAG_FWD_SPARSE_MFMA)
+        assert _lib.workspace_bytes(p) == _lib.workspace_bytes(_p(mask_format=_lib.MASK_2_4, r=r))
 
 
 def test_alignment(lib):

@@ -94,3 +94,24 @@ def test_full_size_straight_through_sampled(name):
     e_da = relerr(dA[:, torch.from_numpy(cols).cuda()].double().cpu().numpy(), olors.ste_da_cols(dY, X, B, s, cols))
     print(name, "straight-through", {"dB": e_db, "dA": e_da}, flush=True)
     assert e_db <= TOL["bf16"] and e_da <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("name", ["llama2_7b_up_proj_2_4", "llama2_13b_gate_proj_2_4"])
+def test_full_size_sparse_mfma_forward_sampled(name):
+    """The structured-sparse forward at full size, in the launch
+    configuration of ``bench.py --sparse-mfma``: sampled outputs against the
+    oracle's entry-wise forward."""
+    wl = synth.workload(name)
+    inp = synth.make(wl)
+    layer = LayerStep(inp, sparse_mfma=True)
+    layer.forward()
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(wl.seed + 7)
+    tok = _sample(rng, wl.L, 5)
+    outs = _sample(rng, wl.R, 255)
+    f = obf16.to_f64
+    got = layer.Y[torch.from_numpy(tok).cuda()][:, torch.from_numpy(outs).cuda()].double().cpu().numpy()
+    ref = olors.forward_entries(f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), wl.scale, tok, outs)
+    err = relerr(got, ref)
+    print(name, "sparse-MFMA forward", err, flush=True)
+    assert err <= 2e-2

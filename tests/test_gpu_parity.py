@@ -26,22 +26,22 @@ def _inputs(name, **kw):
     return synth.make(wl, L=L)
 
 
-def _run(inp, bias=None, need_dbias=False):
+def _run(inp, bias=None, need_dbias=False, sparse_mfma=False):
     dt = inp.wl.dtype
     X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
     fmt = FMT[inp.wl.mask]
     M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
     bias_t = to_dev(bias, dt) if bias is not None else None
-    Y = ops.forward(X, W, M, B, A, inp.wl.scale, fmt, bias=bias_t)
+    Y = ops.forward(X, W, M, B, A, inp.wl.scale, fmt, bias=bias_t, sparse_mfma=sparse_mfma)
     dX, dB, dA, dbias = ops.backward(dY, X, W, M, B, A, inp.wl.scale, fmt, need_dbias=need_dbias)
     torch.cuda.synchronize()
     return Y, dX, dB, dA, dbias
 
 
-def _check_all(inp, bias=None):
+def _check_all(inp, bias=None, sparse_mfma=False):
     dt = inp.wl.dtype
     b64 = to_f64(bias, dt) if bias is not None else None
-    Y, dX, dB, dA, dbias = _run(inp, bias, need_dbias=bias is not None)
+    Y, dX, dB, dA, dbias = _run(inp, bias, need_dbias=bias is not None, sparse_mfma=sparse_mfma)
     rY, rdX, rdB, rdA, rdbias = oracle_full(inp, inp.wl.scale, b64)
     tol = TOL[dt]
     errs = {
@@ -118,11 +118,39 @@ def test_parity_bitmap(R, C, L, r):
     _check_all(inp)
 
 
-@pytest.mark.parametrize("R,C,L,r", [(520, 776, 300, 16), (1024, 512, 700, 64),
-                                     (512, 512, 256, 64)])  # whole tiles, r = 64
-def test_parity_two_four(R, C, L, r):
+@pytest.mark.parametrize("R,C,L,r", [
+    (520, 776, 300, 16),    # ragged in every dimension
+    (1024, 512, 700, 64),
+    (512, 512, 256, 64),    # whole tiles, r = 64
+    (512, 512, 512, 16),    # whole tiles, r = 16
+    (768, 256, 256, 32),    # whole tiles, r = 32
+    (256, 768, 512, 48),    # whole tiles, r = 48
+    (256, 64, 256, 16),     # a single K-step
+    (520, 776, 300, 5),     # odd rank
+    (264, 1064, 77, 24),    # C % 32 = 8: the last mask word of a row is partly padding
+])
+@pytest.mark.parametrize("sparse_mfma", [False, True], ids=["dense_mfma", "sparse_mfma"])
+def test_parity_two_four(R, C, L, r, sparse_mfma):
     inp = _inputs("llama2_7b_up_proj_2_4", R=R, C=C, L=L, r=r, seed=7 * R + L)
-    _check_all(inp)
+    _check_all(inp, sparse_mfma=sparse_mfma)
+
+
+def test_sparse_mfma_bias_and_identity_probe():
+    """Structured-sparse forward: bias epilogue, and X = I exposing W'^T with
+    exact zeros wherever the 2:4 mask drops an element."""
+    inp = _inputs("llama2_7b_up_proj_2_4", R=264, C=520, L=130, r=16, seed=98)
+    rng = np.random.default_rng(2)
+    bias = synth.f32_to_bf16_bits(rng.standard_normal(264).astype(np.float32))
+    _check_all(inp, bias=bias, sparse_mfma=True)
+    n = 64
+    inp = _inputs("llama2_7b_up_proj_2_4", R=n, C=n, L=n, r=16)
+    one = synth.f32_to_bf16_bits(np.ones(1, np.float32))[0]
+    inp.X = np.where(np.eye(n, dtype=bool), one, np.uint16(0)).astype(np.uint16)
+    Y, _, _, _, _ = _run(inp, sparse_mfma=True)
+    Yt = dev_to_f64(Y).T
+    assert np.all(Yt[inp.M == 0] == 0.0)
+    Wp = olors.merged_weight(to_f64(inp.W, "bf16"), inp.M, to_f64(inp.B, "bf16"), to_f64(inp.A, "bf16"), 2.0)
+    assert relerr(Yt, Wp) <= 1e-2
 
 
 def test_parity_seventy_percent():
