@@ -16,7 +16,8 @@
  * derivative of the forward); the mask multiplies the whole sum W + s.B.A;
  * masking is a select, so masked entries are +0; the mask stays on the weight
  * gradient (exact gradient).  The paper's straight-through, re-associated
- * backward (Section 2.3) is reserved under LORS_FLAG_BWD_STE.
+ * backward (Section 2.3) is the LORS_FLAG_BWD_STE variant, and a 2:4 forward
+ * on the structured-sparse MFMA is the LORS_FLAG_FWD_SPARSE_MFMA variant.
  *
  * Names: B is R x r and A is r x C.  The paper calls the R x r adapter
  * (calligraphic) A and the r x C adapter (calligraphic) B; this header uses
