@@ -12,16 +12,23 @@
 //
 //   * prep_kernel: B^T (so that Q's second operand is K-contiguous like A)
 //     and the zeroing of dB and dA, which the contraction accumulates into.
-//   * rows_kernel: P and Q in one launch (grid y selects which).  A
-//     workgroup owns 32 tokens; its four waves split the contraction over K
-//     (C for P, R for Q) into four contiguous ranges and add their partial
-//     tiles through LDS.  Operands go from global memory into registers in
-//     double-buffered batches, so each wave has one batch in flight while it
-//     multiplies the previous one; the token rows are read in whole cache
-//     lines and re-laid through LDS into the MFMA layout.  P and Q are
-//     rounded to bf16 and stored with the rank padded to a multiple of 32
-//     (pad columns zero), which makes every token row of them 64-byte
-//     aligned for the contraction's LDS copies.
+//   * rows_kernel / rows_staged_kernel: P and Q in one launch (grid y
+//     selects which).  A workgroup owns 32 tokens and its four waves add
+//     their partial tiles through LDS.  rows_kernel: the waves split the
+//     contraction over K (C for P, R for Q) into four contiguous ranges, and
+//     operands go from global memory into registers in double-buffered
+//     batches, the token rows in whole cache lines re-laid through LDS into
+//     the MFMA layout; its adapter-side loads touch 32 rows per instruction,
+//     which is cheap for one 32-rank block and limits it beyond that.
+//     rows_staged_kernel: both operands stream through a ring of LDS stages
+//     (128 k of every row per stage, asynchronous copies of whole 256-byte
+//     row segments, one barrier per stage) and the waves split each stage's
+//     k range; it is taken for ranks above 32 when a row is at least 8192
+//     long, where it measured 1.4x to 1.8x faster (at 4096-long rows the
+//     register form still led).  P and Q are rounded to bf16 and stored
+//     with the rank padded to a multiple of 32 (pad columns zero), which
+//     makes every token row of them 64-byte aligned for the contraction's
+//     LDS copies.
 //   * contract_kernel: out[i][j] += s . sum over tokens of U[l][i] V[l][j],
 //     dB tiles (U = dY, V = P) and dA tiles (U = X, V = Q) in one grid.  A
 //     workgroup owns 256 rows i and a slice of the tokens; both operands are
@@ -201,6 +208,124 @@ __global__ __launch_bounds__(NT) void rows_kernel(const uint16_t* __restrict__ X
 }
 
 // ---------------------------------------------------------------------------
+// P and Q through a ring of LDS stages.  Stage: U [32 tokens][KS] and
+// V [RP][KS] (KS = 128 k, 256-byte row segments); the 16-byte chunk c of
+// segment row q is stored at chunk c ^ (q & 15), so the MFMA-layout reads
+// (32 rows, one chunk each) fall on distinct banks.  Each 1 KiB copy fills
+// four segment rows; the waves take equal shares of the copies and a
+// quarter of each stage's k range.
+// ---------------------------------------------------------------------------
+constexpr int SK = 128;                  // k per stage
+constexpr int SROW = 2 * SK;             // bytes per staged row
+constexpr int SCH = SROW / 16;           // chunks per staged row
+constexpr int SRPC = 1024 / SROW;        // staged rows per copy
+constexpr int SUB = 32 * SROW;           // U stage bytes
+
+template <int RK32>
+struct StagedCfg {
+    static constexpr int RP = 32 * RK32;
+    static constexpr int VB = RP * SROW;                 // V stage bytes
+    static constexpr int SB = SUB + VB;                  // one stage
+    static constexpr int NS = 131072 / SB < 6 ? 131072 / SB : 6;  // ring depth within 128 KiB
+    static constexpr int UC = SUB / 4096, VC = VB / 4096;  // copies per wave per stage
+    static constexpr int CPS = UC + VC;
+    static_assert(SUB % 4096 == 0 && VB % 4096 == 0, "copies split evenly over the four waves");
+    static_assert(NS >= 3 && RK32 * 16384 <= NS * SB, "ring depth; the reduction reuses the ring");
+};
+
+template <int RK32>
+__global__ __launch_bounds__(NT) void rows_staged_kernel(const uint16_t* __restrict__ X,
+                                                         const uint16_t* __restrict__ A,
+                                                         const uint16_t* __restrict__ dY,
+                                                         const uint16_t* __restrict__ BT, uint16_t* __restrict__ P,
+                                                         uint16_t* __restrict__ Q, int64_t L, int R, int C, int r) {
+    using Cfg = StagedCfg<RK32>;
+    constexpr int RP = Cfg::RP, NS = Cfg::NS, SB = Cfg::SB, UC = Cfg::UC, VC = Cfg::VC;
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[NS * SB];
+    const bool isq = blockIdx.y == 1;
+    const uint16_t* U = isq ? dY : X;
+    const uint16_t* V = isq ? BT : A;
+    uint16_t* out = isq ? Q : P;
+    const int K = isq ? R : C;
+    const int lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t t0 = (int64_t)blockIdx.x * 32;
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+    const void* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
+    const int nst = (K + SK - 1) / SK;
+    // Lane of a copy: staged row lane / SCH of the copy's SRPC rows, stored
+    // chunk lane % SCH, which holds logical chunk (lane % SCH) ^ (row & 15).
+    // Rows past L or r and chunks past K (K % 8 == 0) read the zero page.
+    const int crow = lane / SCH, pch = lane % SCH;
+    auto issue = [&](int st) {
+        const int k0 = (st < nst ? st : nst - 1) * SK;  // past the end: repeat the last stage (never read)
+        const uint32_t base = lds0 + (uint32_t)((st % NS) * SB);
+#pragma unroll
+        for (int q = 0; q < UC; ++q) {
+            const int blk = UC * wave + q, row = SRPC * blk + crow;
+            const int k = k0 + 8 * (pch ^ (row & 15));
+            const bool ok = t0 + row < L && k < K;
+            copy16_to_lds(ok ? (const void*)(U + (t0 + row) * K + k) : zsrc, base + 1024 * blk);
+        }
+#pragma unroll
+        for (int q = 0; q < VC; ++q) {
+            const int blk = VC * wave + q, row = SRPC * blk + crow;
+            const int k = k0 + 8 * (pch ^ (row & 15));
+            const bool ok = row < r && k < K;
+            copy16_to_lds(ok ? (const void*)(V + (int64_t)row * K + k) : zsrc, base + SUB + 1024 * blk);
+        }
+    };
+    f32x16 acc[RK32];
+#pragma unroll
+    for (int jb = 0; jb < RK32; ++jb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[jb][v] = 0.f;
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) issue(st);
+    for (int st = 0; st < nst; ++st) {
+        stage_barrier<(NS - 2) * Cfg::CPS>();  // stage st landed; stage st - 1 is no longer read
+        issue(st + NS - 1);
+        const uint8_t* sb = smem + (st % NS) * SB;
+#pragma unroll
+        for (int ks = 0; ks < SK / 64; ++ks) {  // this wave's quarter: 16-k steps of 32 k
+            const int c = (SK / 4 * wave + 16 * ks) / 8 + h;  // logical chunk of this lane
+            const bf16x8 a = *(const bf16x8*)(sb + l32 * SROW + ((c ^ (l32 & 15)) << 4));
+#pragma unroll
+            for (int jb = 0; jb < RK32; ++jb) {
+                const int j = 32 * jb + l32;
+                const bf16x8 b = *(const bf16x8*)(sb + SUB + j * SROW + ((c ^ (j & 15)) << 4));
+                acc[jb] = mfma_32x32x16(a, b, acc[jb]);
+            }
+        }
+    }
+    wait_vmcnt<0>();  // the repeated tail stages still land in the ring
+    lds_barrier();
+    float* red = (float*)smem;  // [4 waves][RK32][16][64]
+#pragma unroll
+    for (int jb = 0; jb < RK32; ++jb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) red[((wave * RK32 + jb) * 16 + v) * 64 + lane] = acc[jb][v];
+    __syncthreads();
+    // as in rows_kernel: wave w adds up accumulator elements 4w .. 4w+3
+    const int64_t tr0 = t0 + 8 * wave + 4 * h;
+#pragma unroll
+    for (int jb = 0; jb < RK32; ++jb) {
+        const int j = 32 * jb + l32;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int v = 4 * wave + q;
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) sum += red[((w * RK32 + jb) * 16 + v) * 64 + lane];
+            if (tr0 + q < L) out[(tr0 + q) * RP + j] = j < r ? bf16_bits(sum) : (uint16_t)0;
+        }
+    }
+}
+
+// Row length from which the staged form is taken for ranks above 32.
+constexpr int64_t kStagedMinK = 8192;
+
+// ---------------------------------------------------------------------------
 // out (fp32, atomics) += s . U^T V over the tokens [t0, t1) of grid.y's slice.
 //   U: L x BIG token-major bf16, V: L x RP token-major bf16
 //   TRANS_OUT = false: out[i * r + j] (dB, R x r); true: out[j * BIG + i] (dA, r x C)
@@ -374,8 +499,17 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     uint16_t* P = (uint16_t*)a.ste_ws;
     uint16_t* Q = (uint16_t*)((uint8_t*)a.ste_ws + pq);
     uint16_t* BT = (uint16_t*)((uint8_t*)a.ste_ws + 2 * pq);
-    hipLaunchKernelGGL((rows_kernel<RK32>), dim3((unsigned)((a.L + 31) / 32), 2), dim3(NT), 0, st, X, A, dY,
-                       (const uint16_t*)BT, P, Q, a.L, (int)a.R, (int)a.C, (int)a.r);
+    const dim3 rgrid((unsigned)((a.L + 31) / 32), 2);
+    bool staged = false;
+    if constexpr (RK32 > 1) {
+        staged = a.R >= kStagedMinK || a.C >= kStagedMinK;
+        if (staged)
+            hipLaunchKernelGGL((rows_staged_kernel<RK32>), rgrid, dim3(NT), 0, st, X, A, dY, (const uint16_t*)BT, P,
+                               Q, a.L, (int)a.R, (int)a.C, (int)a.r);
+    }
+    if (!staged)
+        hipLaunchKernelGGL((rows_kernel<RK32>), rgrid, dim3(NT), 0, st, X, A, dY, (const uint16_t*)BT, P, Q, a.L,
+                           (int)a.R, (int)a.C, (int)a.r);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // Token slices: about two workgroups per CU over both products, at

@@ -349,6 +349,11 @@ def test_split_backward_with_mask_reuse(kind):
     ("llama2_7b_q_proj", 512, 264, 260, 128),       # largest rank
     ("llama2_7b_up_proj_2_4", 1024, 512, 700, 40),
     ("llama2_7b_q_proj", 1032, 520, 1, 24),         # single token
+    # rows of 8192 or more with ranks above 32 take the LDS-staged row
+    # products: two, three and four rank blocks, ragged stage tails
+    ("llama2_7b_q_proj", 8200, 264, 100, 40),
+    ("llama2_7b_q_proj", 264, 8200, 77, 96),
+    ("llama2_7b_q_proj", 8192, 136, 33, 128),
 ])
 def test_parity_straight_through(name, R, C, L, r):
     inp = _inputs(name, R=R, C=C, L=L, r=r, seed=3 * R + L + r)
