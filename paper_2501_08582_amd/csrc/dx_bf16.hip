@@ -33,6 +33,7 @@ constexpr int BM = 256;  // tokens per tile
 constexpr int BN = 256;  // input features per tile (64 per wave)
 constexpr int BK = 64;   // output features (rows of W) per K-step
 constexpr int GROUP_M = 4;
+constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
 constexpr int DB = BM * kRow64;      // dY slab: 32 KiB
 constexpr int WB = BK * kRowBytes;   // W slab [k][n]: 32 KiB
@@ -48,6 +49,7 @@ struct Layout {
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NB = (2 * RK + 3) / 4;    // B-slab copies per wave (r/8 copies in all)
     static constexpr int COPIES = 16 + NB + 2;     // copies per wave per stage
+    static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -244,8 +246,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const int nb = p >> 2, q = p & 3;
         wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
     };
+    // late_*: the copies kEarly.. of the stage in the other buffer, issued in
+    // the merge slots of the first sub-step of a K-step (see the main loop)
     auto substep = [&](const bf16x8 (&dc)[8], const u32x4 (&wc)[2], bf16x8 (&dn)[8], u32x4 (&wn)[2],
-                       const uint8_t* sb, int c4n, auto rank_tag) {
+                       const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
+                       bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
         mm(0, dc, wc); read_rs(sb, c4n); SLOT_END();
         mm(1, dc, wc); if constexpr (RANK) read_bfr(sb, 1); SLOT_END();
@@ -258,6 +263,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, dc, wc);
             merge_piece(wn, p, c4n & 1);
+            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, dc, wc);
@@ -285,7 +291,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const int st = kt & 1;
         const uint8_t* sb = smem + st * Lay::STAGE;
         const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
-        substep(da, wa, db, wb, sb, 1, std::true_type{});
+        // copies kEarly.. of stage kt+1 (buffer st^1, free since the last
+        // barrier; the barrier below waits for them); at kt = 0 the prologue
+        // issued all of stage 1
+        const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+        substep(da, wa, db, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
         substep(db, wb, da, wa, sb, 2, std::false_type{});
         substep(da, wa, db, wb, sb, 3, std::false_type{});
         stage_barrier<0>();
@@ -302,12 +312,9 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, db, wb);
             merge_piece(wa, p, 0);
-            if (12 + p < Lay::COPIES) copy_j(12 + p, k2, sq);
             SLOT_END();
         }
         mm(15, db, wb);
-#pragma unroll
-        for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
         SLOT_END();
     }
     // ---- epilogue: round to bf16, stage the wave's 256 x 64 block in LDS

@@ -23,8 +23,11 @@
 // merge arithmetic.  The rank-r product of the second half of a K-step is
 // formed during sub-step 0.  One barrier per K-step, before sub-step 3:
 // after it the next stage is visible and the current one is free, so
-// sub-step 3 interleaves the copies of stage kt+2 and the first sub-step of
-// stage kt+1 with its MFMAs.  X, W, A and mask slabs travel HBM -> LDS with
+// sub-step 3 interleaves the first twelve copies of stage kt+2 and the first
+// sub-step of stage kt+1 with its MFMAs; the remaining copies of that stage
+// go out in the merge slots of the next K-step's sub-step 0, still a K-step
+// ahead of the barrier that waits for them.  A wave stalls on a burst of
+// asynchronous copies, so spreading them keeps the matrix pipe fed.  X, W, A and mask slabs travel HBM -> LDS with
 // global_load_lds; accumulators (256 x 64 per wave) live in AGPRs.
 #include "gemm_common.hpp"
 #include "kernels.hpp"
@@ -39,6 +42,7 @@ constexpr int BM = 256;   // tokens per tile
 constexpr int BN = 256;   // output features per tile (64 per wave)
 constexpr int BK = 64;    // input features per K-step
 constexpr int GROUP_M = 4;
+constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
 constexpr int XB = BM * kRow64;  // 32 KiB
 constexpr int WB = BN * kRow64;  // 32 KiB
@@ -54,6 +58,7 @@ struct Layout {
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NAW = (2 * RK + 3) / 4;  // A-slab copies per wave
     static constexpr int COPIES = 16 + NAW + 2;   // copies per wave per stage
+    static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -256,8 +261,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     };
     // an ordinary sub-step: MFMAs on (xc, wc) while preparing (xn, wn) for
     // sub-step c4n of the stage at sb; optionally the rank-r block of k half 1
+    // late_*: the copies kEarly.. of the stage in the other buffer, issued in
+    // the merge slots of the first sub-step of a K-step (see the main loop)
     auto substep = [&](const bf16x8 (&xc)[8], const u32x4 (&wc)[2], bf16x8 (&xn)[8], u32x4 (&wn)[2],
-                       const uint8_t* sb, int c4n, auto rank_tag) {
+                       const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
+                       bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
         mm(0, xc, wc); read_rs(sb, c4n); SLOT_END();
         mm(1, xc, wc); if constexpr (RANK) read_afr(sb, 1); SLOT_END();
@@ -270,6 +278,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xc, wc);
             merge_piece(wn, p, c4n & 1);
+            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, xc, wc);
@@ -299,7 +308,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const int st = kt & 1;
         const uint8_t* sb = smem + st * Lay::STAGE;
         const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
-        substep(xa, wa, xb, wb, sb, 1, std::true_type{});
+        // copies kEarly.. of stage kt+1 (buffer st^1, free since the last
+        // barrier; the barrier below waits for them); at kt = 0 the prologue
+        // issued all of stage 1
+        const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+        substep(xa, wa, xb, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
         substep(xb, wb, xa, wa, sb, 2, std::false_type{});
         substep(xa, wa, xb, wb, sb, 3, std::false_type{});
         // sub-step 3: stage kt+1 landed everywhere, stage kt free
@@ -317,12 +330,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xb, wb);
             merge_piece(wa, p, 0);
-            if (12 + p < Lay::COPIES) copy_j(12 + p, k2, sq);
             SLOT_END();
         }
         mm(15, xb, wb);
-#pragma unroll
-        for (int j = 20; j < Lay::COPIES; ++j) copy_j(j, k2, sq);
         SLOT_END();
     }
     // ---- epilogue: (+bias), round to bf16, stage the wave's 256 x 64 block in
