@@ -32,6 +32,9 @@ constexpr int STAGEB = 2 * TILEB;      // dY slab + X slab
 constexpr int SMEM = 2 * STAGEB;       // two stages
 constexpr int GROUP_M = 4;
 constexpr int LOADS = TILEB / 1024 / (NT / kWave);  // 1 KiB copies per wave per slab (8)
+// copy pairs of a stage issued right after the barrier; the rest go out a
+// sub-step later (a wave stalls on a burst of asynchronous copies)
+constexpr int kEarlyPairs = 4;
 
 // Epilogue LDS carve-up (reuses the stage buffers; EP_A lies past them).
 constexpr int GT_PITCH = 512;                      // G^T tile: [j][i], 256 i per row
@@ -136,10 +139,12 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     // c+1 are read from LDS while the 16 MFMAs of sub-step c run.  One
     // barrier per K-step, before its last sub-step: after it every wave has
     // finished reading the current stage and the next stage has landed, so
-    // the last sub-step interleaves its MFMAs with the copies of stage kt+2
-    // (into the buffer just consumed) and the first fragment reads of stage
-    // kt+1.  The body has no data-dependent branches: at the tail the copies
-    // repeat the last K-slab into a buffer that is never read again.
+    // the last sub-step interleaves its MFMAs with the first kEarlyPairs copy
+    // pairs of stage kt+2 (into the buffer just consumed) and the first
+    // fragment reads of stage kt+1; the remaining pairs of stage kt+2 go out
+    // during sub-step 0 of the next K-step.  The body has no data-dependent
+    // branches besides the first K-step's: at the tail the copies repeat the
+    // last K-slab into a buffer that is never read again.
     static_assert(BK / 16 == 4 && LOADS == 8, "sub-step schedule below assumes 4 sub-steps, 8 copy pairs");
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -166,8 +171,28 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
         const int st = (int)(kt & 1);
         const uint8_t* sb = smem + st * STAGEB;
         const uint8_t* sn = smem + (st ^ 1) * STAGEB;
-        load_frags(fa1, fb1, sb, 1);
-        mfma16(fa0, fb0);
+        {
+            // sub-step 0, with the transpose reads of sub-step 1 and copy
+            // pairs kEarlyPairs.. of stage kt+1 interleaved (that stage's
+            // buffer, st^1, is free since the last barrier, and the barrier
+            // below waits for the copies; at kt = 0 the prologue issued all
+            // of stage 1)
+            const int64_t k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+            const uint32_t sq1 = lds0 + (st ^ 1) * STAGEB;
+            const uint8_t* s1 = sb + 16 * kRowBytes;
+            u32x2 lo = {0u, 0u};
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int f = i >> 2, part = i & 3;
+                acc[f][part] = mfma_32x32x16(fa0[f], fb0[part], acc[f][part]);
+                if (part == 0) lo = lds_tr_read(s1 + offA[f][0]);
+                if (part == 1) fa1[f] = frag_from_tr(lo, lds_tr_read(s1 + offA[f][1]));
+                if (part == 2) lo = lds_tr_read(s1 + offB[f][0]);
+                if (part == 3) fb1[f] = frag_from_tr(lo, lds_tr_read(s1 + offB[f][1]));
+                if (kt > 0 && part == 1 && kEarlyPairs + f < LOADS) copy_pair(kEarlyPairs + f, k1, sq1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
         load_frags(fa0, fb0, sb, 2);
         mfma16(fa1, fb1);
         load_frags(fa1, fb1, sb, 3);
@@ -179,7 +204,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
         for (int i = 0; i < 16; ++i) {
             const int a = i >> 2, b = i & 3;
             acc[a][b] = mfma_32x32x16(fa1[a], fb1[b], acc[a][b]);
-            if ((i & 1) == 0) copy_pair(i >> 1, k0, sbq);
+            if ((i & 1) == 0 && (i >> 1) < kEarlyPairs) copy_pair(i >> 1, k0, sbq);
             if (i < 8) {
                 // fragment i/2 of A (even i) or B (odd i) of sub-step 0, stage kt+1
                 if ((i & 1) == 0)
