@@ -319,17 +319,20 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         stage_barrier<0>();
         const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
         const uint32_t sq = lds0 + st * Lay::STAGE;
+        // one copy per MFMA slot: a copy issued behind an MFMA stalls the
+        // wave while that MFMA runs, a second one would stall the next
         mm(0, xb, wb); read_mw(sn); read_afr(sn, 0); copy_j(0, k2, sq); SLOT_END();
-        mm(1, xb, wb); copy_j(1, k2, sq); copy_j(2, k2, sq); SLOT_END();
-        mm(2, xb, wb); read_x2(xa, sn, 0, 0); copy_j(3, k2, sq); copy_j(4, k2, sq); SLOT_END();
-        mm(3, xb, wb); read_x2(xa, sn, 0, 1); copy_j(5, k2, sq); copy_j(6, k2, sq); SLOT_END();
-        mm(4, xb, wb); read_rs(sn, 0); copy_j(7, k2, sq); copy_j(8, k2, sq); SLOT_END();
-        mm(5, xb, wb); read_x2(xa, sn, 0, 2); copy_j(9, k2, sq); copy_j(10, k2, sq); SLOT_END();
-        mm(6, xb, wb); read_x2(xa, sn, 0, 3); rank_mfma2<RK>(T, afr, bfr); copy_j(11, k2, sq); SLOT_END();
+        mm(1, xb, wb); copy_j(1, k2, sq); SLOT_END();
+        mm(2, xb, wb); read_x2(xa, sn, 0, 0); copy_j(2, k2, sq); SLOT_END();
+        mm(3, xb, wb); read_x2(xa, sn, 0, 1); copy_j(3, k2, sq); SLOT_END();
+        mm(4, xb, wb); read_rs(sn, 0); copy_j(4, k2, sq); SLOT_END();
+        mm(5, xb, wb); read_x2(xa, sn, 0, 2); copy_j(5, k2, sq); SLOT_END();
+        mm(6, xb, wb); read_x2(xa, sn, 0, 3); rank_mfma2<RK>(T, afr, bfr); copy_j(6, k2, sq); SLOT_END();
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xb, wb);
             merge_piece(wa, p, 0);
+            if (7 + p < kEarly) copy_j(7 + p, k2, sq);
             SLOT_END();
         }
         mm(15, xb, wb);
