@@ -59,6 +59,7 @@ struct Layout {
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NAW = (2 * RK + 3) / 4;
     static constexpr int COPIES = 16 + NAW + 2;
+    static_assert(COPIES - 16 <= 8, "the late copies fit the even slots of a half-step");
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -243,17 +244,26 @@ __global__ __launch_bounds__(NT, 1) void fwd24_kernel(
     bf16x16 xh[8];         // X operands of half 1, all read during half 0 (before the barrier)
     u32x4 wa[2], wb[2];    // compressed W' operands of alternate half-steps
     uint32_t ia[2], ib[2]; // their index operands
+    // the first MFMA holds the last operands of a previous half-step as well
+    xh[7] = bf16x16{};
+    wb[1] = zero_u32x4();
+    ib[1] = 0u;
     f32x16 T;              // rank-r block of the feature block being prepared
     uint32_t mw[2][2];     // mask words [nb][kb] of the stage being prepared
     u32x4 raw[2];          // raw W [c] of that feature block
     u32x2 psel[2];         // permute selectors [c]
     bf16x8 afr[RK];
 
-    auto smf = [&](int i, const bf16x16& xf, const u32x4 (&wf)[2], const uint32_t (&ix)[2]) {
+    // kx, kw, ki: the operands of the previous structured-sparse MFMA.  The
+    // matrix core reads its sources over several passes after issue, so they
+    // are held here, as inputs of the next one, and no instruction in
+    // between may reuse their registers.
+    auto smf = [&](int i, const bf16x16& xf, const u32x4 (&wf)[2], const uint32_t (&ix)[2], const bf16x16& kx,
+                   const u32x4& kw, uint32_t ki) {
         const int mb = i >> 1, nb = i & 1;
         asm volatile("v_smfmac_f32_32x32x32_bf16 %0, %1, %2, %3\n\ts_nop 7"
                      : "+a"(acc[nb][mb])
-                     : "v"(wf[nb]), "v"(xf), "v"(ix[nb]));
+                     : "v"(wf[nb]), "v"(xf), "v"(ix[nb]), "v"(kx), "v"(kw), "v"(ki));
     };
     auto read_afr = [&](const uint8_t* sb, int kb) {
 #pragma unroll
@@ -294,45 +304,46 @@ __global__ __launch_bounds__(NT, 1) void fwd24_kernel(
     // Half-step 0 of a K-step: MFMAs of half 0 (X from the ring, block mb + 2
     // read at slot 2 mb) while reading all X operands of half 1 and preparing
     // its W' operand, one feature block at a time.  Every read of the stage
-    // happens here, before the barrier.
-    auto half0 = [&](const uint8_t* sb) {
-        smf(0, xr[0], wa, ia); read_x(xr[2], sb, 0, 2); read_afr(sb, 1); SLOT_END();
-        smf(1, xr[0], wa, ia); read_blk(sb, 1, 0, ib); read_x(xh[0], sb, 1, 0); SLOT_END();
-        smf(2, xr[1], wa, ia); read_x(xr[3], sb, 0, 3); rank_mfma1<RK>(T, afr, bfr[0]); SLOT_END();
-        smf(3, xr[1], wa, ia); read_x(xh[1], sb, 1, 1); piece(wb, 0, 0); SLOT_END();
-        smf(4, xr[2], wa, ia); read_x(xr[0], sb, 0, 4); piece(wb, 0, 1); SLOT_END();
-        smf(5, xr[2], wa, ia); read_x(xh[2], sb, 1, 2); piece(wb, 0, 2); SLOT_END();
-        smf(6, xr[3], wa, ia); read_x(xr[1], sb, 0, 5); piece(wb, 0, 3); SLOT_END();
-        smf(7, xr[3], wa, ia); read_blk(sb, 1, 1, ib); read_x(xh[3], sb, 1, 3); SLOT_END();
-        smf(8, xr[0], wa, ia); read_x(xr[2], sb, 0, 6); rank_mfma1<RK>(T, afr, bfr[1]); SLOT_END();
-        smf(9, xr[0], wa, ia); read_x(xh[4], sb, 1, 4); piece(wb, 1, 0); SLOT_END();
-        smf(10, xr[1], wa, ia); read_x(xr[3], sb, 0, 7); piece(wb, 1, 1); SLOT_END();
-        smf(11, xr[1], wa, ia); read_x(xh[5], sb, 1, 5); piece(wb, 1, 2); SLOT_END();
-        smf(12, xr[2], wa, ia); read_x(xh[6], sb, 1, 6); piece(wb, 1, 3); SLOT_END();
-        smf(13, xr[2], wa, ia); read_x(xh[7], sb, 1, 7); SLOT_END();
-        smf(14, xr[3], wa, ia); SLOT_END();
-        smf(15, xr[3], wa, ia); SLOT_END();
+    // happens here, before the barrier.  cp(t) issues this slot's late
+    // copies of the next stage.
+    auto half0 = [&](const uint8_t* sb, auto cp) {
+        smf(0, xr[0], wa, ia, xh[7], wb[1], ib[1]); read_x(xr[2], sb, 0, 2); read_afr(sb, 1); cp(0); SLOT_END();
+        smf(1, xr[0], wa, ia, xr[0], wa[0], ia[0]); read_blk(sb, 1, 0, ib); read_x(xh[0], sb, 1, 0); cp(1); SLOT_END();
+        smf(2, xr[1], wa, ia, xr[0], wa[1], ia[1]); read_x(xr[3], sb, 0, 3); rank_mfma1<RK>(T, afr, bfr[0]); cp(2); SLOT_END();
+        smf(3, xr[1], wa, ia, xr[1], wa[0], ia[0]); read_x(xh[1], sb, 1, 1); piece(wb, 0, 0); cp(3); SLOT_END();
+        smf(4, xr[2], wa, ia, xr[1], wa[1], ia[1]); read_x(xr[0], sb, 0, 4); piece(wb, 0, 1); cp(4); SLOT_END();
+        smf(5, xr[2], wa, ia, xr[2], wa[0], ia[0]); read_x(xh[2], sb, 1, 2); piece(wb, 0, 2); cp(5); SLOT_END();
+        smf(6, xr[3], wa, ia, xr[2], wa[1], ia[1]); read_x(xr[1], sb, 0, 5); piece(wb, 0, 3); cp(6); SLOT_END();
+        smf(7, xr[3], wa, ia, xr[3], wa[0], ia[0]); read_blk(sb, 1, 1, ib); read_x(xh[3], sb, 1, 3); cp(7); SLOT_END();
+        smf(8, xr[0], wa, ia, xr[3], wa[1], ia[1]); read_x(xr[2], sb, 0, 6); rank_mfma1<RK>(T, afr, bfr[1]); cp(8); SLOT_END();
+        smf(9, xr[0], wa, ia, xr[0], wa[0], ia[0]); read_x(xh[4], sb, 1, 4); piece(wb, 1, 0); cp(9); SLOT_END();
+        smf(10, xr[1], wa, ia, xr[0], wa[1], ia[1]); read_x(xr[3], sb, 0, 7); piece(wb, 1, 1); cp(10); SLOT_END();
+        smf(11, xr[1], wa, ia, xr[1], wa[0], ia[0]); read_x(xh[5], sb, 1, 5); piece(wb, 1, 2); cp(11); SLOT_END();
+        smf(12, xr[2], wa, ia, xr[1], wa[1], ia[1]); read_x(xh[6], sb, 1, 6); piece(wb, 1, 3); cp(12); SLOT_END();
+        smf(13, xr[2], wa, ia, xr[2], wa[0], ia[0]); read_x(xh[7], sb, 1, 7); cp(13); SLOT_END();
+        smf(14, xr[3], wa, ia, xr[2], wa[1], ia[1]); cp(14); SLOT_END();
+        smf(15, xr[3], wa, ia, xr[3], wa[0], ia[0]); cp(15); SLOT_END();
     };
     // Half-step 1: MFMAs of half 1 (X from xh) while preparing half 0 of the
     // next stage at sn (ring blocks 0, 1 and its W' operand); cp(t) issues
     // this slot's copies of stage kt+2.
     auto half1 = [&](const uint8_t* sn, auto cp) {
-        smf(0, xh[0], wb, ib); read_mw(sn); read_afr(sn, 0); cp(0); SLOT_END();
-        smf(1, xh[0], wb, ib); read_blk(sn, 0, 0, ia); cp(1); SLOT_END();
-        smf(2, xh[1], wb, ib); rank_mfma1<RK>(T, afr, bfr[0]); cp(2); SLOT_END();
-        smf(3, xh[1], wb, ib); piece(wa, 0, 0); cp(3); SLOT_END();
-        smf(4, xh[2], wb, ib); piece(wa, 0, 1); cp(4); SLOT_END();
-        smf(5, xh[2], wb, ib); piece(wa, 0, 2); cp(5); SLOT_END();
-        smf(6, xh[3], wb, ib); piece(wa, 0, 3); cp(6); SLOT_END();
-        smf(7, xh[3], wb, ib); read_blk(sn, 0, 1, ia); cp(7); SLOT_END();
-        smf(8, xh[4], wb, ib); rank_mfma1<RK>(T, afr, bfr[1]); cp(8); SLOT_END();
-        smf(9, xh[4], wb, ib); piece(wa, 1, 0); cp(9); SLOT_END();
-        smf(10, xh[5], wb, ib); piece(wa, 1, 1); cp(10); SLOT_END();
-        smf(11, xh[5], wb, ib); piece(wa, 1, 2); cp(11); SLOT_END();
-        smf(12, xh[6], wb, ib); piece(wa, 1, 3); read_x(xr[0], sn, 0, 0); cp(12); SLOT_END();
-        smf(13, xh[6], wb, ib); read_x(xr[1], sn, 0, 1); cp(13); SLOT_END();
-        smf(14, xh[7], wb, ib); cp(14); SLOT_END();
-        smf(15, xh[7], wb, ib); cp(15); SLOT_END();
+        smf(0, xh[0], wb, ib, xr[3], wa[1], ia[1]); read_mw(sn); read_afr(sn, 0); cp(0); SLOT_END();
+        smf(1, xh[0], wb, ib, xh[0], wb[0], ib[0]); read_blk(sn, 0, 0, ia); cp(1); SLOT_END();
+        smf(2, xh[1], wb, ib, xh[0], wb[1], ib[1]); rank_mfma1<RK>(T, afr, bfr[0]); cp(2); SLOT_END();
+        smf(3, xh[1], wb, ib, xh[1], wb[0], ib[0]); piece(wa, 0, 0); cp(3); SLOT_END();
+        smf(4, xh[2], wb, ib, xh[1], wb[1], ib[1]); piece(wa, 0, 1); cp(4); SLOT_END();
+        smf(5, xh[2], wb, ib, xh[2], wb[0], ib[0]); piece(wa, 0, 2); cp(5); SLOT_END();
+        smf(6, xh[3], wb, ib, xh[2], wb[1], ib[1]); piece(wa, 0, 3); cp(6); SLOT_END();
+        smf(7, xh[3], wb, ib, xh[3], wb[0], ib[0]); read_blk(sn, 0, 1, ia); cp(7); SLOT_END();
+        smf(8, xh[4], wb, ib, xh[3], wb[1], ib[1]); rank_mfma1<RK>(T, afr, bfr[1]); cp(8); SLOT_END();
+        smf(9, xh[4], wb, ib, xh[4], wb[0], ib[0]); piece(wa, 1, 0); cp(9); SLOT_END();
+        smf(10, xh[5], wb, ib, xh[4], wb[1], ib[1]); piece(wa, 1, 1); cp(10); SLOT_END();
+        smf(11, xh[5], wb, ib, xh[5], wb[0], ib[0]); piece(wa, 1, 2); cp(11); SLOT_END();
+        smf(12, xh[6], wb, ib, xh[5], wb[1], ib[1]); piece(wa, 1, 3); read_x(xr[0], sn, 0, 0); cp(12); SLOT_END();
+        smf(13, xh[6], wb, ib, xh[6], wb[0], ib[0]); read_x(xr[1], sn, 0, 1); cp(13); SLOT_END();
+        smf(14, xh[7], wb, ib, xh[6], wb[1], ib[1]); cp(14); SLOT_END();
+        smf(15, xh[7], wb, ib, xh[7], wb[0], ib[0]); cp(15); SLOT_END();
     };
     // prepare half 0 of the stage at sb without MFMAs (prologue)
     auto prepare = [&](const uint8_t* sb) {
@@ -364,16 +375,21 @@ __global__ __launch_bounds__(NT, 1) void fwd24_kernel(
         const int st = kt & 1;
         const uint8_t* sb = smem + st * Lay::STAGE;
         const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
-        half0(sb);
+        // copies 16.. of stage kt+1 (buffer st^1, free since the last barrier;
+        // the barrier below waits for them); at kt = 0 the prologue issued
+        // all of stage 1
+        const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+        const uint32_t sq1 = lds0 + (st ^ 1) * Lay::STAGE;
+        half0(sb, [&](int t) {
+            if (kt > 0 && (t & 1) == 0 && 16 + t / 2 < Lay::COPIES) copy_j(16 + t / 2, k1, sq1);
+        });
         // stage kt+1 landed everywhere; every read of stage kt is done
         stage_barrier<0>();
         const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
         const uint32_t sq = lds0 + st * Lay::STAGE;
-        half1(sn, [&](int t) {
-            const int j0 = 2 * t;
-            if (j0 < Lay::COPIES) copy_j(j0, k2, sq);
-            if (j0 + 1 < Lay::COPIES) copy_j(j0 + 1, k2, sq);
-        });
+        // one copy per MFMA slot: a second copy behind the same MFMA would
+        // stall the wave past it
+        half1(sn, [&](int t) { copy_j(t, k2, sq); });
     }
     // ---- epilogue: (+bias), round to bf16, stage the wave's 256 tokens x 64
     // features block in LDS (rows of 64 outputs), then 16-byte row stores
