@@ -3,7 +3,10 @@
 
 One step = lors_forward + lors_backward_data + lors_backward_weight over one
 batch of seeded synthetic inputs already resident in HBM (every step of the
-layer runs in liblors.so; mask packing happens once, before timing).
+layer runs in liblors.so; mask packing happens once, before timing).  With
+--graph the step is captured once as a HIP graph and replayed (a replay must
+reproduce the eager step first); by default the library calls are issued from
+Python every step.
 
 Prints ONE JSON line: whole-job TFLOP/s over the algorithmic flops
 6RCL + 8rRC per step, the fraction of the bf16 MFMA peak, peak bytes, the
@@ -45,6 +48,9 @@ def parse():
                          "flops counted are those of that method")
     ap.add_argument("--sparse-mfma", action="store_true",
                     help="2:4 workloads: forward on the structured-sparse MFMA")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay one captured HIP graph of the step instead of issuing the library calls "
+                         "from Python every step (per-kernel timings are eager either way)")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="short program for hardware-counter runs: one step, a device copy of "
                          "COPY_BYTES (the calibration of the byte counters), one more step")
@@ -165,6 +171,38 @@ def main():
         step()
     torch.cuda.synchronize()
 
+    launch = "eager"
+    if args.graph:
+        # One step captured as a HIP graph (the library allocates nothing and
+        # records no memset), replayed K times; a replay must reproduce the
+        # eager step's outputs before anything is timed.
+        outs = (layer.Y, layer.dX, layer.dB, layer.dA)
+        ref = [t.clone() for t in outs]
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        for t in outs:
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        exact = all(torch.equal(a, b) for a, b in zip(outs[:2], ref[:2]))
+        close = all(float((a.double() - b.double()).norm()) <= 1e-5 * float(b.double().norm()) + 1e-30
+                    for a, b in zip(outs[2:], ref[2:]))  # fp32 atomics: summation order varies
+        if not (exact and close):
+            print("bench.py: the graph replay does not reproduce the eager step", file=sys.stderr)
+            sys.exit(1)
+        step = graph.replay  # noqa: F811
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        launch = "hip graph replay"
+
     # Timed region: K steps bracketed by a device synchronisation on both
     # sides, HIP events on the launch stream at its two ends only.
     torch.cuda.reset_peak_memory_stats()
@@ -230,7 +268,8 @@ def main():
         "config": {"workload": wl.name, "R": R, "C": C, "L": L, "r": r, "mask": wl.mask,
                    "sparsity": wl.sparsity, "scale": s,
                    "weight_gradient": "straight-through" if args.ste else "exact masked",
-                   "forward_mfma": "structured-sparse" if args.sparse_mfma else "dense"},
+                   "forward_mfma": "structured-sparse" if args.sparse_mfma else "dense",
+                   "step_launch": launch},
         "pct_mfma_peak": round(100.0 * value / peak, 2),
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),
