@@ -385,3 +385,28 @@ def test_straight_through_equals_exact_for_a_dense_mask():
     torch.cuda.synchronize()
     assert relerr(dev_to_f64(dB_s), dev_to_f64(dB_e)) <= 1e-2
     assert relerr(dev_to_f64(dA_s), dev_to_f64(dA_e)) <= 1e-2
+
+
+# ---------------------------------------------------------------------------
+# seeded shapes at every rank-bucket edge of the kernels (16-wide rank blocks,
+# the wide path above 64), ragged in R, C and L, both mask kinds
+# ---------------------------------------------------------------------------
+def _edge_cases():
+    rng = np.random.default_rng(2501)
+    ranks = [1, 15, 16, 17, 31, 32, 33, 48, 49, 63, 64, 65, 100, 128]
+    out = []
+    for i, r in enumerate(ranks):
+        R = 8 * int(rng.integers(1, 140))
+        C = 8 * int(rng.integers(1, 140))
+        L = int(rng.integers(1, 700))
+        out.append((R, C, L, r, "2:4" if i % 2 else "magnitude"))
+    return out
+
+
+@pytest.mark.parametrize("R,C,L,r,mask", _edge_cases())
+def test_parity_rank_bucket_edges(R, C, L, r, mask):
+    name = "llama2_7b_up_proj_2_4" if mask == "2:4" else "llama2_7b_q_proj"
+    inp = _inputs(name, R=R, C=C, L=L, r=r, seed=R * 131 + C * 7 + L + r)
+    _check_all(inp)
+    if mask == "2:4" and r <= 64:
+        _check_all(inp, sparse_mfma=True)
