@@ -93,6 +93,19 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 
 __device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }
 
+// Eight bf16 sums a + b (pairs packed in 32-bit words), each rounded once to
+// bf16 from the fp32 sum.
+__device__ __forceinline__ u32x4 add_bf16x8(u32x4 a, u32x4 b) {
+    u32x4 o;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const float lo = __uint_as_float(a[p] << 16) + __uint_as_float(b[p] << 16);
+        const float hi = __uint_as_float(a[p] & 0xFFFF0000u) + __uint_as_float(b[p] & 0xFFFF0000u);
+        o[p] = pack_bf16x2(lo, hi);
+    }
+    return o;
+}
+
 // 16-bit element e (0..7) of a 16-byte vector.
 __device__ __forceinline__ uint32_t u16_at(u32x4 v, int e) {
     return (v[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;

@@ -57,12 +57,14 @@ struct Layout {
 // RAGGED: some tile reaches past L, C or R (copies check every lane and read
 // the zero page outside the tensors); otherwise copies use uniform bases plus
 // fixed per-lane offsets.
-template <int RK, bool RAGGED>
+// PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
+// taken as zero and the product is added onto dX.  ldb: row stride of B.
+template <int RK, bool RAGGED, bool PASS2>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
-    float s, int tiles_m, int tiles_n) {
+    float s, int tiles_m, int tiles_n, int ldb) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -83,8 +85,17 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const int wprT = (R + 31) >> 5;  // words per row of M^T
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
-    const int slab_b = 2 * r;        // bytes per B row
+    const int slab_b = 2 * r;        // bytes per B row in the slab
     const int nbcopies = r >> 3;     // 1 KiB copies per B slab (64 rows x 2r bytes)
+    // B-slab copy q of this wave: its 16 bytes are row brow[q], byte bcol[q]
+    // of the [64][r] slab; rows of B are ldb elements apart in memory
+    int brow[Lay::NB], bcol[Lay::NB];
+#pragma unroll
+    for (int q = 0; q < Lay::NB; ++q) {
+        const int off = 1024 * (4 * q + wave) + 16 * lane;
+        brow[q] = off / slab_b;
+        bcol[q] = off - brow[q] * slab_b;
+    }
 
     // M^T is a plain bitmap whatever the caller's layout.
     *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
@@ -145,6 +156,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 copy16_to_lds(ok ? (const void*)(Dt + (int64_t)row * R + k0 + 8 * lc) : (const void*)zsrc, dst);
             }
         } else if (j < 16) {
+            if (PASS2) return;  // W is zero: its slabs were cleared once
             const int q = j - 8, blk = 8 * wave + q;
             const uint32_t dst = sb + Lay::W + 1024 * blk;
             if constexpr (!RAGGED) {
@@ -158,12 +170,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         } else if (j < 16 + Lay::NB) {
             // B rows k0 .. k0+63 are one contiguous block; every wave issues
             // NB copies, those past the block go to the sink
-            const int blk = 4 * (j - 16) + wave;
+            const int q = j - 16, blk = 4 * q + wave;
             const bool real = blk < nbcopies;
-            const int off = 1024 * blk + 16 * lane;   // byte offset inside the slab
-            const bool ok = real && (!RAGGED || k0 + off / slab_b < R);
-            copy16_to_lds(ok ? (const void*)((const uint8_t*)Bm + (int64_t)k0 * slab_b + off) : (const void*)zsrc,
-                          real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
+            const bool ok = real && (!RAGGED || k0 + brow[q] < R);
+            const void* src = (const uint8_t*)Bm + ((int64_t)k0 + brow[q]) * (2 * (int64_t)ldb) + bcol[q];
+            copy16_to_lds(ok ? src : (const void*)zsrc, real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
         } else {
             const int q = j - 16 - Lay::NB;
             const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
@@ -271,6 +282,12 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         SLOT_END();
     };
 
+    if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
+        for (int i = tid; i < 2 * (WB / 16); i += NT)
+            *(u32x4*)(smem + (i / (WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (WB / 16))) = zero_u32x4();
+        __syncthreads();
+    }
+
     // ---- prologue: stages 0 and 1 in flight, then sub-step 0 of stage 0
 #pragma unroll
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
@@ -338,12 +355,17 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
         const int64_t gm = m0 + row;
         const int gn = n0 + 64 * wave + 8 * ch;
-        if (gm < L && gn < C) *(u32x4*)(dX + gm * C + gn) = v;
+        if (gm < L && gn < C) {
+            if constexpr (PASS2)
+                *(u32x4*)(dX + gm * C + gn) = add_bf16x8(*(const u32x4*)(dX + gm * C + gn), v);
+            else
+                *(u32x4*)(dX + gm * C + gn) = v;
+        }
     }
 }
 
-template <int RK>
-hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
+template <int RK, bool PASS2>
+hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
@@ -359,26 +381,42 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     auto* A = (const uint16_t*)a.A;
     auto* dX = (uint16_t*)a.dX;
     if (ragged)
-        hipLaunchKernelGGL((dx_kernel<RK, true>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((dx_kernel<RK, true, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
+                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
     else
-        hipLaunchKernelGGL((dx_kernel<RK, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
+                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
     return hipGetLastError();
+}
+
+hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb) {
+    switch ((a.r + 15) / 16) {
+        case 1: return pass2 ? launch_rk<1, true>(a, st, ldb) : launch_rk<1, false>(a, st, ldb);
+        case 2: return pass2 ? launch_rk<2, true>(a, st, ldb) : launch_rk<2, false>(a, st, ldb);
+        case 3: return pass2 ? launch_rk<3, true>(a, st, ldb) : launch_rk<3, false>(a, st, ldb);
+        case 4: return pass2 ? launch_rk<4, true>(a, st, ldb) : launch_rk<4, false>(a, st, ldb);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0 || a.dX == nullptr) return hipSuccess;
-    if (a.r % 8 != 0 || a.Mt == nullptr) return launch_dx_bf16_wide(a, st);
-    switch ((a.r + 15) / 16) {
-        case 1: return launch_rk<1>(a, st);
-        case 2: return launch_rk<2>(a, st);
-        case 3: return launch_rk<3>(a, st);
-        case 4: return launch_rk<4>(a, st);
-        default: return launch_dx_bf16_wide(a, st);
-    }
+    if (a.r % 8 != 0 || a.Mt == nullptr || a.r > 128) return launch_dx_bf16_wide(a, st);
+    if (a.r <= 64) return launch_ranks(a, st, false, (int)a.r);
+    // Ranks above 64: two passes over the ranks [0, 64) and [64, r), the
+    // second with W taken as zero and its product added onto dX (the mask
+    // distributes over the sum; one more bf16 rounding of dX).
+    LayerArgs a1 = a;
+    a1.r = 64;
+    const hipError_t e = launch_ranks(a1, st, false, (int)a.r);
+    if (e != hipSuccess) return e;
+    LayerArgs a2 = a;
+    a2.r = a.r - 64;
+    a2.B = (const uint16_t*)a.B + 64;
+    a2.A = (const uint16_t*)a.A + 64 * a.C;
+    return launch_ranks(a2, st, true, (int)a.r);
 }
 
 }  // namespace lors

@@ -66,13 +66,15 @@ struct Layout {
 // RAGGED: some tile reaches past L, R or C (copies then check every lane and
 // read the zero page outside the tensors); otherwise every slab row and
 // K-chunk is in range and copies use a uniform base plus fixed offsets.
-template <int RK, bool TWO_FOUR, bool RAGGED>
+// PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
+// taken as zero and the product is added onto Y.  ldb: row stride of B.
+template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2>
 __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, const uint16_t* __restrict__ bias,
     uint16_t* __restrict__ Y, int64_t L, int R, int C, int r, float s, int tiles_m,
-    int tiles_n) {
+    int tiles_n, int ldb) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -97,7 +99,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // and the resident B operand of the merge: column n = 64 wave + 32 nb + l32,
     // ranks 16c + 8h .. +7
     *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<TWO_FOUR>((uint32_t)tid);
-    const bool b_vec = (r & 7) == 0;
+    const bool b_vec = (r & 7) == 0 && (ldb & 7) == 0;
     bf16x8 bfr[2][RK];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             u32x4 v = zero_u32x4();
             const int j0 = 16 * c + 8 * h;
             if (gn < R) {
-                const uint16_t* src = Bm + (int64_t)gn * r + j0;
+                const uint16_t* src = Bm + (int64_t)gn * ldb + j0;
                 if (b_vec) {
                     if (j0 < r) v = *(const u32x4*)src;
                 } else {
@@ -155,6 +157,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         if (j < 16) {
             const int q = j & 7;
             const bool isx = j < 8;
+            if (PASS2 && !isx) return;  // W is zero: its slabs were cleared once
             const uint32_t dst = sb + (isx ? Lay::X : Lay::W) + 1024 * (8 * wave + q);
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr((isx ? Xt : Wt) + k0), offXW[q], dst);
@@ -286,6 +289,12 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         SLOT_END();
     };
 
+    if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
+        for (int i = tid; i < 2 * (WB / 16); i += NT)
+            *(u32x4*)(smem + (i / (WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (WB / 16))) = zero_u32x4();
+        __syncthreads();
+    }
+
     // ---- prologue: stages 0 and 1 in flight, then sub-step 0 of stage 0
 #pragma unroll
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
@@ -359,12 +368,17 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
         const int64_t gm = m0 + row;
         const int gn = n0 + 64 * wave + 8 * ch;
-        if (gm < L && gn < R) *(u32x4*)(Y + gm * R + gn) = v;
+        if (gm < L && gn < R) {
+            if constexpr (PASS2)
+                *(u32x4*)(Y + gm * R + gn) = add_bf16x8(*(const u32x4*)(Y + gm * R + gn), v);
+            else
+                *(u32x4*)(Y + gm * R + gn) = v;
+        }
     }
 }
 
-template <int RK, bool TWO_FOUR>
-hipError_t launch_fmt(const LayerArgs& a, hipStream_t st) {
+template <int RK, bool TWO_FOUR, bool PASS2>
+hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.R + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
@@ -379,31 +393,52 @@ hipError_t launch_fmt(const LayerArgs& a, hipStream_t st) {
     // 32 bits
     const bool ragged = a.L % BM != 0 || a.R % BN != 0 || a.C % BK != 0 || (int64_t)BM * a.C * 2 >= (1ll << 31);
     if (ragged)
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
+                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
     else
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false>), grid, block, 0, st, X, W, a.M, B, A, bias, Y, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
+                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
     return hipGetLastError();
 }
 
 template <int RK>
-hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
+hipError_t launch_rk(const LayerArgs& a, hipStream_t st, bool pass2, int ldb) {
     if (a.two_four && a.sparse_mfma) return launch_fwd24_bf16(a, st);  // structured-sparse MFMA
-    return a.two_four ? launch_fmt<RK, true>(a, st) : launch_fmt<RK, false>(a, st);
+    if (pass2) return a.two_four ? launch_fmt<RK, true, true>(a, st, ldb) : launch_fmt<RK, false, true>(a, st, ldb);
+    return a.two_four ? launch_fmt<RK, true, false>(a, st, ldb) : launch_fmt<RK, false, false>(a, st, ldb);
+}
+
+hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb) {
+    switch ((a.r + 15) / 16) {
+        case 1: return launch_rk<1>(a, st, pass2, ldb);
+        case 2: return launch_rk<2>(a, st, pass2, ldb);
+        case 3: return launch_rk<3>(a, st, pass2, ldb);
+        case 4: return launch_rk<4>(a, st, pass2, ldb);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0) return hipSuccess;
-    switch ((a.r + 15) / 16) {
-        case 1: return launch_rk<1>(a, st);
-        case 2: return launch_rk<2>(a, st);
-        case 3: return launch_rk<3>(a, st);
-        case 4: return launch_rk<4>(a, st);
-        default: return launch_fwd_bf16_wide(a, st);
-    }
+    if (a.r <= 64) return launch_ranks(a, st, false, (int)a.r);
+    if (a.r % 8 != 0 || a.r > 128) return launch_fwd_bf16_wide(a, st);
+    // Ranks above 64: the mask distributes over the sum, so
+    //   W' = select(M, W + s.B1.A1, 0) + select(M, s.B2.A2, 0)
+    // for ranks [0, 64) and [64, r): two passes of the register-merge
+    // kernel, the second with W taken as zero, no bias, and its product added
+    // onto Y (one more bf16 rounding of Y).
+    LayerArgs a1 = a;
+    a1.r = 64;
+    const hipError_t e = launch_ranks(a1, st, false, (int)a.r);
+    if (e != hipSuccess) return e;
+    LayerArgs a2 = a;
+    a2.r = a.r - 64;
+    a2.B = (const uint16_t*)a.B + 64;
+    a2.A = (const uint16_t*)a.A + 64 * a.C;
+    a2.bias = nullptr;
+    return launch_ranks(a2, st, true, (int)a.r);
 }
 
 }  // namespace lors

@@ -410,3 +410,36 @@ def test_parity_rank_bucket_edges(R, C, L, r, mask):
     _check_all(inp)
     if mask == "2:4" and r <= 64:
         _check_all(inp, sparse_mfma=True)
+
+
+# ---------------------------------------------------------------------------
+# ranks above 64 that are multiples of 8 run as two passes of the 64-rank
+# kernels (the second with W taken as zero, added onto Y and dX)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,L,r,mask", [
+    (520, 776, 300, 96, "magnitude"),   # ragged, second pass r = 32
+    (264, 1032, 77, 72, "2:4"),         # second pass r = 8
+    (768, 512, 513, 128, "magnitude"),  # second pass r = 64, one token past a tile
+    (512, 768, 512, 80, "2:4"),         # whole tiles (fixed-offset copies)
+])
+def test_parity_two_pass_ranks(R, C, L, r, mask):
+    name = "llama2_7b_up_proj_2_4" if mask == "2:4" else "llama2_7b_q_proj"
+    inp = _inputs(name, R=R, C=C, L=L, r=r, seed=R + 3 * C + L + r)
+    _check_all(inp)
+
+
+def test_parity_two_pass_bias_and_straight_through():
+    inp = _inputs("llama2_7b_q_proj", R=264, C=520, L=130, r=112, seed=99)
+    rng = np.random.default_rng(5)
+    bias = synth.f32_to_bf16_bits(rng.standard_normal(264).astype(np.float32))
+    _check_all(inp, bias=bias)
+    dt = inp.wl.dtype
+    X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    fmt = FMT[inp.wl.mask]
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
+    dX, dB, dA, _ = ops.backward(dY, X, W, M, B, A, inp.wl.scale, fmt, ste=True)
+    torch.cuda.synchronize()
+    f = lambda a: to_f64(a, dt)  # noqa: E731
+    rdX, rdB, rdA = olors.backward_ste(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), inp.wl.scale)
+    for got, ref in ((dX, rdX), (dB, rdB), (dA, rdA)):
+        assert relerr(dev_to_f64(got), ref) <= TOL[dt]
