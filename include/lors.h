@@ -37,7 +37,7 @@
  * rounded once to bf16 (nearest-even) before the main product; all products
  * accumulate in fp32; Y and dX are rounded to bf16 (nearest-even); G is
  * rounded to bf16 before the two rank-r products; dA, dB, dbias stay fp32.
- * For 64 < r <= 128 with r % 8 == 0 the forward and dX use that the mask
+ * For 64 < r <= 128 the forward (and dX when r % 8 == 0) use that the mask
  * distributes over the adapter's rank blocks: Y (and dX) is the bf16 sum of
  * the product with select(M, W + s.B[:, :64].A[:64, :]) and the product with
  * select(M, s.B[:, 64:].A[64:, :]), each merged weight rounded once, so Y and

@@ -423,7 +423,7 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb)
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0) return hipSuccess;
     if (a.r <= 64) return launch_ranks(a, st, false, (int)a.r);
-    if (a.r % 8 != 0 || a.r > 128) return launch_fwd_bf16_wide(a, st);
+    if (a.r > 128) return hipErrorInvalidValue;  // the problem check caps r at 128
     // Ranks above 64: the mask distributes over the sum, so
     //   W' = select(M, W + s.B1.A1, 0) + select(M, s.B2.A2, 0)
     // for ranks [0, 64) and [64, r): two passes of the register-merge

@@ -32,7 +32,6 @@ struct LayerArgs {
 
 // bf16 path
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
-hipError_t launch_fwd_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_fwd24_bf16(const LayerArgs& a, hipStream_t s);      // 2:4 mask, sparse MFMA, rank <= 64
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_dx_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
