@@ -37,7 +37,7 @@
  * rounded once to bf16 (nearest-even) before the main product; all products
  * accumulate in fp32; Y and dX are rounded to bf16 (nearest-even); G is
  * rounded to bf16 before the two rank-r products; dA, dB, dbias stay fp32.
- * For 64 < r <= 128 the forward (and dX when r % 8 == 0) use that the mask
+ * For 64 < r <= 128 the forward and dX use that the mask
  * distributes over the adapter's rank blocks: Y (and dX) is the bf16 sum of
  * the product with select(M, W + s.B[:, :64].A[:64, :]) and the product with
  * select(M, s.B[:, 64:].A[64:, :]), each merged weight rounded once, so Y and
@@ -198,7 +198,9 @@ lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C
  * the mask, 4 * C * ceil(R/32) bytes rounded up to 256 (about R*C/8, i.e.
  * 1/16 of W), plus with LORS_FLAG_BWD_STE the P and Q buffers (2*L*rp
  * bytes each, rp = r rounded up to a multiple of 32) and B^T (2*r*R bytes),
- * each rounded up to 256; 0 for fp32.
+ * plus, when r is not a multiple of 8, a copy of B whose rows are padded with
+ * zeros to r8 = r rounded up to a multiple of 8 (2*R*r8 bytes), each part
+ * rounded up to 256; 0 for fp32.
  * (size_t)-1 if p is invalid.  The workspace must be
  * 16-byte aligned, must not overlap any argument, and is overwritten; its
  * contents on return are unspecified.  lors_forward needs no workspace. */

@@ -102,20 +102,29 @@ size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
     return static_cast<size_t>(R * words_per_row(C) * 4);
 }
 
-// bf16 backward: the transposed bitmap M^T (C rows of ceil(R/32) words),
-// rounded up to 256 bytes.  The forward and the fp32 path need nothing.
-// bf16 workspace: the transposed mask bitmap, then (straight-through flag)
-// the P, Q and B^T buffers of the re-associated adapter gradients.
+// bf16 backward workspace, each part rounded up to 256 bytes: the
+// transposed bitmap M^T (C rows of ceil(R/32) words); with the
+// straight-through flag, the P, Q and B^T buffers of the re-associated
+// adapter gradients; for ranks that are not a multiple of 8, a copy of B
+// with its rows padded to roundup8(r) zero-filled columns, so that the dX
+// kernel copies whole 16-byte chunks.  The forward and the fp32 path need
+// nothing.
 static size_t mt_bytes(const lors_problem_t* p) {
     const int64_t bytes = p->C * ((p->R + 31) / 32) * 4;
     return static_cast<size_t>((bytes + 255) / 256 * 256);
 }
+static size_t ste_bytes(const lors_problem_t* p) {
+    return (p->flags & LORS_FLAG_BWD_STE) != 0u ? lors::ste_workspace_bytes(p->R, p->L, p->r) : 0;
+}
+static int64_t padded_rank(int64_t r) { return (r + 7) / 8 * 8; }
+static size_t bpad_bytes(const lors_problem_t* p) {
+    if (p->r % 8 == 0) return 0;
+    return static_cast<size_t>((2 * p->R * padded_rank(p->r) + 255) / 256 * 256);
+}
 size_t lors_workspace_bytes(const lors_problem_t* p) {
     if (p == nullptr || check_problem(p) != LORS_OK) return static_cast<size_t>(-1);
     if (p->dtype != LORS_DTYPE_BF16) return 0;
-    size_t n = mt_bytes(p);
-    if ((p->flags & LORS_FLAG_BWD_STE) != 0u) n += lors::ste_workspace_bytes(p->R, p->L, p->r);
-    return n;
+    return mt_bytes(p) + ste_bytes(p) + bpad_bytes(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -316,6 +325,9 @@ lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* 
     a.reuse_mt = (p->flags & LORS_FLAG_REUSE_MASK_T) != 0u;
     a.ste = (p->flags & LORS_FLAG_BWD_STE) != 0u;
     a.ste_ws = (a.ste && workspace) ? static_cast<uint8_t*>(workspace) + mt_bytes(p) : nullptr;
+    a.b_pad = (p->dtype == LORS_DTYPE_BF16 && bpad_bytes(p) && workspace)
+                  ? static_cast<uint8_t*>(workspace) + mt_bytes(p) + ste_bytes(p)
+                  : nullptr;
     return a;
 }
 

@@ -59,12 +59,14 @@ struct Layout {
 // fixed per-lane offsets.
 // PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
 // taken as zero and the product is added onto dX.  ldb: row stride of B.
+// r: the rank the kernel works on, a multiple of 8 (B's columns ra .. r-1
+// are zero); ra: the rows of A that exist (A rows ra .. r-1 are read as zero).
 template <int RK, bool RAGGED, bool PASS2>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
-    float s, int tiles_m, int tiles_n, int ldb) {
+    int ra, float s, int tiles_m, int tiles_n, int ldb) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const int row = 2 * blk + h;
         const int lc = swz_chunk(row, lane & 31);
         const int gn = n0 + 8 * lc;
-        copy16_to_lds((row < r && gn < C) ? (const void*)(Am + (int64_t)row * C + gn) : (const void*)zsrc,
+        copy16_to_lds((row < ra && gn < C) ? (const void*)(Am + (int64_t)row * C + gn) : (const void*)zsrc,
                       lds0 + Lay::STAGE + 1024 * blk);
     }
     stage_barrier<0>();
@@ -365,7 +367,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 }
 
 template <int RK, bool PASS2>
-hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb) {
+hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
@@ -382,19 +384,20 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb) {
     auto* dX = (uint16_t*)a.dX;
     if (ragged)
         hipLaunchKernelGGL((dx_kernel<RK, true, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb);
     else
         hipLaunchKernelGGL((dx_kernel<RK, false, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb);
     return hipGetLastError();
 }
 
-hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb) {
+// a.r: the (padded) rank of this pass; ra: the rows of A that exist
+hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb, int ra) {
     switch ((a.r + 15) / 16) {
-        case 1: return pass2 ? launch_rk<1, true>(a, st, ldb) : launch_rk<1, false>(a, st, ldb);
-        case 2: return pass2 ? launch_rk<2, true>(a, st, ldb) : launch_rk<2, false>(a, st, ldb);
-        case 3: return pass2 ? launch_rk<3, true>(a, st, ldb) : launch_rk<3, false>(a, st, ldb);
-        case 4: return pass2 ? launch_rk<4, true>(a, st, ldb) : launch_rk<4, false>(a, st, ldb);
+        case 1: return pass2 ? launch_rk<1, true>(a, st, ldb, ra) : launch_rk<1, false>(a, st, ldb, ra);
+        case 2: return pass2 ? launch_rk<2, true>(a, st, ldb, ra) : launch_rk<2, false>(a, st, ldb, ra);
+        case 3: return pass2 ? launch_rk<3, true>(a, st, ldb, ra) : launch_rk<3, false>(a, st, ldb, ra);
+        case 4: return pass2 ? launch_rk<4, true>(a, st, ldb, ra) : launch_rk<4, false>(a, st, ldb, ra);
         default: return hipErrorInvalidValue;
     }
 }
@@ -403,20 +406,32 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb)
 
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0 || a.dX == nullptr) return hipSuccess;
-    if (a.r % 8 != 0 || a.Mt == nullptr || a.r > 128) return launch_dx_bf16_wide(a, st);
-    if (a.r <= 64) return launch_ranks(a, st, false, (int)a.r);
+    if (a.Mt == nullptr || a.r < 1 || a.r > 128) return hipErrorInvalidValue;
+    // The B slab is copied in whole 16-byte chunks of its rows.  A rank that
+    // is not a multiple of 8 works on a copy of B whose rows are padded with
+    // zero columns to rp = roundup8(r); the missing A rows are read as zero.
+    LayerArgs ap = a;
+    const int rp = (int)((a.r + 7) / 8 * 8);
+    if (rp != a.r) {
+        if (a.b_pad == nullptr) return hipErrorInvalidValue;
+        const hipError_t e = launch_pad_cols_bf16(a.B, a.R, a.r, rp, a.b_pad, st);
+        if (e != hipSuccess) return e;
+        ap.B = a.b_pad;
+        ap.r = rp;
+    }
+    if (rp <= 64) return launch_ranks(ap, st, false, rp, (int)a.r);
     // Ranks above 64: two passes over the ranks [0, 64) and [64, r), the
     // second with W taken as zero and its product added onto dX (the mask
     // distributes over the sum; one more bf16 rounding of dX).
-    LayerArgs a1 = a;
+    LayerArgs a1 = ap;
     a1.r = 64;
-    const hipError_t e = launch_ranks(a1, st, false, (int)a.r);
+    const hipError_t e = launch_ranks(a1, st, false, rp, 64);
     if (e != hipSuccess) return e;
-    LayerArgs a2 = a;
-    a2.r = a.r - 64;
-    a2.B = (const uint16_t*)a.B + 64;
+    LayerArgs a2 = ap;
+    a2.r = rp - 64;
+    a2.B = (const uint16_t*)ap.B + 64;
     a2.A = (const uint16_t*)a.A + 64 * a.C;
-    return launch_ranks(a2, st, true, (int)a.r);
+    return launch_ranks(a2, st, true, rp, (int)a.r - 64);
 }
 
 }  // namespace lors

@@ -28,13 +28,13 @@ struct LayerArgs {
     float* dbias;           // R or nullptr
     bool ste;               // straight-through adapter gradients (Section 2.3)
     void* ste_ws;           // P, Q, B^T scratch of the straight-through path
+    void* b_pad;            // R x roundup8(r) scratch for B when r % 8 != 0 (bf16 backward), else nullptr
 };
 
 // bf16 path
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_fwd24_bf16(const LayerArgs& a, hipStream_t s);      // 2:4 mask, sparse MFMA, rank <= 64
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
-hipError_t launch_dx_bf16_wide(const LayerArgs& a, hipStream_t s);  // any rank <= 128
 hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_ste_bf16(const LayerArgs& a, hipStream_t s);  // dB, dA of the straight-through backward
 size_t ste_workspace_bytes(int64_t R, int64_t L, int64_t r);
@@ -48,6 +48,8 @@ hipError_t launch_dbias_f32(const LayerArgs& a, hipStream_t s);
 
 // helpers
 hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t s);
+// out (R x rp, bf16) = B (R x r) with its columns r .. rp-1 set to zero
+hipError_t launch_pad_cols_bf16(const void* B, int64_t R, int64_t r, int64_t rp, void* out, hipStream_t s);
 // clears two fp32 buffers with one launch
 hipError_t launch_zero2_f32(float* a, int64_t na, float* b, int64_t nb, hipStream_t s);
 hipError_t launch_mask_pack(const uint8_t* dense, int64_t R, int64_t C, bool two_four,

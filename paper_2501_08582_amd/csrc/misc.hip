@@ -168,6 +168,17 @@ __global__ __launch_bounds__(NT) void zero2_kernel(float* __restrict__ a, int64_
     }
 }
 
+// out[R x rp] = B[R x r] with columns r .. rp-1 zero (bf16 bit patterns).
+__global__ __launch_bounds__(NT) void pad_cols_kernel(const uint16_t* __restrict__ B, int64_t R, int r, int rp,
+                                                      uint16_t* __restrict__ out) {
+    const int64_t n = R * rp, stride = (int64_t)gridDim.x * NT;
+    for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < n; t += stride) {
+        const int64_t i = t / rp;
+        const int j = (int)(t - i * rp);
+        out[t] = j < r ? B[i * r + j] : (uint16_t)0;
+    }
+}
+
 // dbias[R] = column sums of dY[L x R]; thread owns one column and a slice of
 // rows, partial sums are combined with fp32 atomics (dbias zeroed first).
 template <bool BF16>
@@ -265,6 +276,16 @@ hipError_t launch_zero2_f32(float* a, int64_t na, float* b, int64_t nb, hipStrea
     const int64_t want = (n + NT - 1) / NT;
     const unsigned blocks = (unsigned)(want < 2048 ? want : 2048);
     hipLaunchKernelGGL(zero2_kernel, dim3(blocks), dim3(NT), 0, st, a, na, b, nb);
+    return hipGetLastError();
+}
+
+hipError_t launch_pad_cols_bf16(const void* B, int64_t R, int64_t r, int64_t rp, void* out, hipStream_t st) {
+    const int64_t n = R * rp;
+    if (n == 0) return hipSuccess;
+    const int64_t want = (n + NT - 1) / NT;
+    const unsigned blocks = (unsigned)(want < 2048 ? want : 2048);
+    hipLaunchKernelGGL(pad_cols_kernel, dim3(blocks), dim3(NT), 0, st, (const uint16_t*)B, R, (int)r, (int)rp,
+                       (uint16_t*)out);
     return hipGetLastError();
 }
 

@@ -222,18 +222,34 @@ def test_workspace_query(lib):
     assert _lib.workspace_bytes(_p(R=4096, C=14336)) == 14336 * 128 * 4
     assert _lib.workspace_bytes(_p(R=520, C=776)) == -(-776 * 17 * 4 // 256) * 256
     assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32)) == 0
+    assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32, r=5)) == 0
     assert _lib.workspace_bytes(_p(R=0)) == 2**64 - 1
+
+
+def test_workspace_query_padded_rank(lib):
+    # a rank that is not a multiple of 8 adds a copy of B (R rows of
+    # roundup8(r) bf16), rounded up to 256 bytes, after the other parts
+    up = lambda n: -(-n // 256) * 256  # noqa: E731
+    for R, C, r in ((64, 64, 5), (520, 776, 1), (4096, 4096, 4), (512, 512, 100), (512, 512, 127)):
+        mt = up(C * -(-R // 32) * 4)
+        want = mt + up(2 * R * (-(-r // 8) * 8))
+        assert _lib.workspace_bytes(_p(R=R, C=C, r=r)) == want
+    for r in (8, 16, 96, 128):
+        assert _lib.workspace_bytes(_p(r=r)) == 512
 
 
 def test_workspace_query_straight_through(lib):
     # transposed mask, then P and Q (2*L*rp bytes each, rp = r rounded up to
-    # a multiple of 32) and B^T (2*r*R), each rounded up to 256 bytes
+    # a multiple of 32) and B^T (2*r*R), then the padded copy of B when r % 8
+    # != 0, each rounded up to 256 bytes
     up = lambda n: -(-n // 256) * 256  # noqa: E731
     for R, C, L, r in ((64, 64, 32, 8), (520, 776, 300, 5), (4096, 4096, 4096, 16), (4096, 14336, 8192, 64),
                        (512, 512, 77, 100)):
         mt = up(C * -(-R // 32) * 4)
         rp = -(-r // 32) * 32
         want = mt + 2 * up(2 * L * rp) + up(2 * r * R)
+        if r % 8:
+            want += up(2 * R * (-(-r // 8) * 8))
         assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=_lib.FLAG_BWD_STE)) == want
 
 

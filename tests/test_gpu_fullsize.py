@@ -37,7 +37,18 @@ def _sample(rng, n, k):
 
 @pytest.mark.parametrize("name", WORKLOADS)
 def test_full_size_sampled(name):
-    wl = synth.workload(name)
+    _check_sampled(synth.workload(name))
+
+
+@pytest.mark.parametrize("r", [4, 100])
+def test_full_size_padded_rank_sampled(r):
+    """Ranks that are not a multiple of 8 (the backward pads B in the
+    workspace; 100 also splits into two rank passes) at the 4096 x 4096 size."""
+    _check_sampled(synth.workload("llama2_7b_q_proj").with_(r=r))
+
+
+def _check_sampled(wl):
+    name = wl.name
     inp = synth.make(wl)
     layer = LayerStep(inp)
     layer.run()

@@ -389,7 +389,8 @@ def test_straight_through_equals_exact_for_a_dense_mask():
 
 # ---------------------------------------------------------------------------
 # seeded shapes at every rank-bucket edge of the kernels (16-wide rank blocks,
-# the wide path above 64), ragged in R, C and L, both mask kinds
+# two passes above 64, padded B for ranks that are not a multiple of 8),
+# ragged in R, C and L, both mask kinds
 # ---------------------------------------------------------------------------
 def _edge_cases():
     rng = np.random.default_rng(2501)
@@ -443,3 +444,53 @@ def test_parity_two_pass_bias_and_straight_through():
     rdX, rdB, rdA = olors.backward_ste(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), inp.wl.scale)
     for got, ref in ((dX, rdX), (dB, rdB), (dA, rdA)):
         assert relerr(dev_to_f64(got), ref) <= TOL[dt]
+
+
+# ---------------------------------------------------------------------------
+# ranks that are not a multiple of 8: the backward copies B into the
+# workspace with its rows padded to roundup8(r) zero columns
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,L,r,mask", [
+    (520, 776, 300, 4, "magnitude"),    # ragged
+    (264, 1032, 77, 5, "2:4"),
+    (512, 768, 512, 12, "magnitude"),   # whole tiles (fixed-offset copies)
+    (768, 512, 513, 100, "magnitude"),  # two passes: 64, then 36 of 40 padded
+    (512, 512, 256, 127, "2:4"),        # two passes, whole tiles, 63 of 64
+])
+def test_parity_padded_ranks(R, C, L, r, mask):
+    name = "llama2_7b_up_proj_2_4" if mask == "2:4" else "llama2_7b_q_proj"
+    inp = _inputs(name, R=R, C=C, L=L, r=r, seed=2 * R + C + L + r)
+    _check_all(inp)
+
+
+def test_padded_rank_workspace_reuse_and_straight_through():
+    """The padded copy of B is rebuilt on every call: a second backward with
+    a new B in the same workspace, with the mask-reuse flag, gives the dX of
+    the new B; with the straight-through flag the padded copy sits after the
+    P, Q and B^T buffers and every output still matches the oracle."""
+    from paper_2501_08582_amd import _lib
+    R, C, L, r = 520, 776, 300, 5
+    inp = _inputs("llama2_7b_q_proj", R=R, C=C, L=L, r=r, seed=41)
+    X, W, B, A, dY = (to_dev(t, "bf16") for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), ops.BITMAP)
+    p = _lib.problem(R, C, L, r, inp.wl.scale, _lib.DTYPE_BF16, _lib.MASK_BITMAP)
+    pr = _lib.problem(R, C, L, r, inp.wl.scale, _lib.DTYPE_BF16, _lib.MASK_BITMAP, _lib.FLAG_REUSE_MASK_T)
+    nws = _lib.workspace_bytes(p)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    rng = np.random.default_rng(8)
+    B2_bits = synth.f32_to_bf16_bits(rng.standard_normal((R, r)).astype(np.float32))
+    B2 = to_dev(B2_bits, "bf16")
+    f = lambda a: to_f64(a, "bf16")  # noqa: E731
+    for prob, Bt, Bh in ((p, B, inp.B), (pr, B2, B2_bits)):
+        dX = torch.empty((L, C), dtype=torch.bfloat16, device="cuda")
+        _lib.check(_lib.backward_data(prob, dY.data_ptr(), W.data_ptr(), M.data_ptr(), Bt.data_ptr(), A.data_ptr(),
+                                      dX.data_ptr(), ws.data_ptr(), nws, st), "data")
+        torch.cuda.synchronize()
+        rdX = olors.backward(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(Bh), f(inp.A), inp.wl.scale)[0]
+        assert relerr(dev_to_f64(dX), rdX) <= TOL["bf16"]
+    dX, dB, dA, _ = ops.backward(dY, X, W, M, B, A, inp.wl.scale, ops.BITMAP, ste=True)
+    torch.cuda.synchronize()
+    rdX, rdB, rdA = olors.backward_ste(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), inp.wl.scale)
+    for got, ref in ((dX, rdX), (dB, rdB), (dA, rdA)):
+        assert relerr(dev_to_f64(got), ref) <= TOL["bf16"]
