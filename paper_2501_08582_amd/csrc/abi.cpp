@@ -317,6 +317,7 @@ lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* 
                            float* dA, float* dbias, void* workspace) {
     lors::LayerArgs a{};
     a.R = p->R; a.C = p->C; a.L = p->L; a.r = p->r;
+    a.r_grad = p->r;
     a.scale = p->scale;
     a.two_four = p->mask_format == LORS_MASK_2_4;
     a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.dY = dY;
@@ -339,8 +340,11 @@ hipError_t build_mt(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
 }
 
 hipError_t run_weight(const lors::LayerArgs& a, bool bf16, hipStream_t s) {
-    // the straight-through launches clear dB and dA themselves
-    hipError_t e = a.ste ? lors::launch_ste_bf16(a, s) : lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
+    // the straight-through launches clear dB and dA themselves, and so does
+    // the dX launch of the combined backward (a.clear_grads)
+    hipError_t e = a.ste          ? lors::launch_ste_bf16(a, s)
+                   : a.clear_grads ? hipSuccess
+                                   : lors::launch_zero2_f32(a.dB, a.R * a.r, a.dA, a.r * a.C, s);
     if (e == hipSuccess && !a.ste) e = bf16 ? lors::launch_g_bf16(a, s) : lors::launch_g_f32(a, s);
     if (e == hipSuccess) e = bf16 ? lors::launch_dbias_bf16(a, s) : lors::launch_dbias_f32(a, s);
     return e;
@@ -358,9 +362,12 @@ lors_status_t lors_backward(const lors_problem_t* p, const void* dY, const void*
         return LORS_ERR_NULL;
     lors_status_t st = check_backward(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace, workspace_bytes);
     if (st != LORS_OK) return st;
-    const lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace);
+    lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, workspace);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool bf16 = p->dtype == LORS_DTYPE_BF16;
+    // the bf16 dX kernel clears dB and dA for the weight gradient's atomics,
+    // which saves the separate clearing launch
+    a.clear_grads = bf16 && !a.ste && dX != nullptr && tok;
     hipError_t e = build_mt(a, bf16, s);
     if (e == hipSuccess && dX) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
     if (e == hipSuccess) e = run_weight(a, bf16, s);

@@ -66,7 +66,8 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
-    int ra, float s, int tiles_m, int tiles_n, int ldb) {
+    int ra, float s, int tiles_m, int tiles_n, int ldb, float* __restrict__ z0, int64_t nz0,
+    float* __restrict__ z1, int64_t nz1) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -78,6 +79,17 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31;
     const int h = lane >> 5;
+
+    // z0, z1: dB and dA of the combined backward, cleared here for the fp32
+    // atomics of the weight-gradient kernel that follows on the same stream
+    // (one launch fewer; plain stores, grid-stride)
+    if (z0 != nullptr) {
+        const int64_t stride = (int64_t)gridDim.x * NT;
+        for (int64_t t = (int64_t)blockIdx.x * NT + tid; t < nz0 + nz1; t += stride) {
+            if (t < nz0) z0[t] = 0.f;
+            else z1[t - nz0] = 0.f;
+        }
+    }
 
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, tm, tn);
@@ -367,7 +379,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 }
 
 template <int RK, bool PASS2>
-hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra) {
+hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool clear) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
     dim3 grid(tiles_m * tiles_n), block(NT);
@@ -382,22 +394,28 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra) {
     auto* B = (const uint16_t*)a.B;
     auto* A = (const uint16_t*)a.A;
     auto* dX = (uint16_t*)a.dX;
+    // clear: dB (R x rank) and dA (rank x C) of the caller's problem
+    float* z0 = clear ? a.dB : nullptr;
+    float* z1 = clear ? a.dA : nullptr;
+    const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
     if (ragged)
         hipLaunchKernelGGL((dx_kernel<RK, true, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb);
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1);
     else
         hipLaunchKernelGGL((dx_kernel<RK, false, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb);
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1);
     return hipGetLastError();
 }
 
 // a.r: the (padded) rank of this pass; ra: the rows of A that exist
+// The first pass clears dB and dA when the caller asks for it (a.clear_grads).
 hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb, int ra) {
+    const bool c = a.clear_grads && !pass2;
     switch ((a.r + 15) / 16) {
-        case 1: return pass2 ? launch_rk<1, true>(a, st, ldb, ra) : launch_rk<1, false>(a, st, ldb, ra);
-        case 2: return pass2 ? launch_rk<2, true>(a, st, ldb, ra) : launch_rk<2, false>(a, st, ldb, ra);
-        case 3: return pass2 ? launch_rk<3, true>(a, st, ldb, ra) : launch_rk<3, false>(a, st, ldb, ra);
-        case 4: return pass2 ? launch_rk<4, true>(a, st, ldb, ra) : launch_rk<4, false>(a, st, ldb, ra);
+        case 1: return pass2 ? launch_rk<1, true>(a, st, ldb, ra, false) : launch_rk<1, false>(a, st, ldb, ra, c);
+        case 2: return pass2 ? launch_rk<2, true>(a, st, ldb, ra, false) : launch_rk<2, false>(a, st, ldb, ra, c);
+        case 3: return pass2 ? launch_rk<3, true>(a, st, ldb, ra, false) : launch_rk<3, false>(a, st, ldb, ra, c);
+        case 4: return pass2 ? launch_rk<4, true>(a, st, ldb, ra, false) : launch_rk<4, false>(a, st, ldb, ra, c);
         default: return hipErrorInvalidValue;
     }
 }

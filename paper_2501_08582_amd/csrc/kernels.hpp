@@ -29,6 +29,8 @@ struct LayerArgs {
     bool ste;               // straight-through adapter gradients (Section 2.3)
     void* ste_ws;           // P, Q, B^T scratch of the straight-through path
     void* b_pad;            // R x roundup8(r) scratch for B when r % 8 != 0 (bf16 backward), else nullptr
+    bool clear_grads;       // the bf16 dX launch also clears dB and dA (combined backward)
+    int64_t r_grad;         // rank of dB and dA (the caller's r; the dX passes change a.r)
 };
 
 // bf16 path

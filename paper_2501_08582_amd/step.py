@@ -1,11 +1,13 @@
 """One forward + backward pass of the layer on device-resident inputs.
 
 This is the launch configuration the throughput benchmark times and the
-full-size parity tests check: ``lors_forward``, then ``lors_backward_data``
-(which builds the transposed mask in the workspace), then
-``lors_backward_weight`` reusing that mask (``LORS_FLAG_REUSE_MASK_T``), all
-on the current stream.  Every step runs in ``liblors.so``; this module only
-allocates buffers and passes pointers.
+full-size parity tests check: ``lors_forward``, then ``lors_backward`` (dX and
+the adapter gradients in one call), both on the current stream.  The mask is
+frozen, so like its packing, its transposed layout is built once when the
+layer is set up (a ``lors_backward_data`` call writes it into the workspace)
+and every step passes ``LORS_FLAG_REUSE_MASK_T``, as a training loop over
+a sparse layer does from its second step on.  Every step runs in
+``liblors.so``; this module only allocates buffers and passes pointers.
 """
 from __future__ import annotations
 
@@ -65,8 +67,12 @@ class LayerStep:
                       else self.p)
         self.p_reuse = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_REUSE_MASK_T)
         self.p_weight = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_BWD_STE) if ste else self.p_reuse)
+        self.p_bwd = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt,
+                                  _lib.FLAG_REUSE_MASK_T | (_lib.FLAG_BWD_STE if ste else 0))
         self.ws = max(_lib.workspace_bytes(self.p), _lib.workspace_bytes(self.p_weight))
         self.wsbuf = torch.empty(max(self.ws, 1), dtype=torch.uint8, device="cuda")
+        # mask preparation, once per layer: the transposed mask into the workspace
+        self.backward_data()
 
     def _ptrs(self):
         st = torch.cuda.current_stream()
@@ -93,8 +99,16 @@ class LayerStep:
                                         self.B.data_ptr(), self.A.data_ptr(), self.dB.data_ptr(), self.dA.data_ptr(),
                                         None, self.wsbuf.data_ptr(), self.ws, sh), "lors_backward_weight")
 
+    def backward(self) -> None:
+        """dX, dB, dA in one call, reusing the transposed mask (the dX
+        kernel also clears dB and dA for the weight gradient's atomics)."""
+        _, sh = self._ptrs()
+        _lib.check(_lib.backward(self.p_bwd, self.dY.data_ptr(), self.X.data_ptr(), self.W.data_ptr(),
+                                 self.M.data_ptr(), self.B.data_ptr(), self.A.data_ptr(), self.dX.data_ptr(),
+                                 self.dB.data_ptr(), self.dA.data_ptr(), None, self.wsbuf.data_ptr(), self.ws, sh),
+                   "lors_backward")
+
     def run(self) -> None:
-        """One pass: forward, data backward, weight backward."""
+        """One pass: forward, then the backward."""
         self.forward()
-        self.backward_data()
-        self.backward_weight()
+        self.backward()

@@ -494,3 +494,41 @@ def test_padded_rank_workspace_reuse_and_straight_through():
     rdX, rdB, rdA = olors.backward_ste(f(inp.dY), f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), inp.wl.scale)
     for got, ref in ((dX, rdX), (dB, rdB), (dA, rdA)):
         assert relerr(dev_to_f64(got), ref) <= TOL["bf16"]
+
+
+# ---------------------------------------------------------------------------
+# the combined backward clears dB and dA inside its dX launch: outputs that
+# start as NaN are overwritten, a second call does not accumulate onto the
+# first, and the split calls give the same gradients
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,L,r", [(256, 512, 256, 16), (264, 520, 130, 5), (320, 288, 200, 100),
+                                     (512, 256, 512, 64)])
+def test_combined_backward_overwrites_gradients(R, C, L, r):
+    inp = _inputs("llama2_7b_q_proj", R=R, C=C, r=r, seed=900 + r, L=L)
+    X, W, B, A, dY = (to_dev(t, "bf16") for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), ops.BITMAP)
+    s = inp.wl.scale
+    _, _, rdB, rdA, _ = oracle_full(inp, s)
+    dX = torch.empty((L, C), dtype=torch.bfloat16, device="cuda")
+    dB = torch.full((R, r), float("nan"), dtype=torch.float32, device="cuda")
+    dA = torch.full((r, C), float("nan"), dtype=torch.float32, device="cuda")
+    print("combined backward", (R, C, L, r), flush=True)
+    for call in range(2):
+        ops.backward(dY, X, W, M, B, A, s, ops.BITMAP, out=(dX, dB, dA, None))
+        torch.cuda.synchronize()
+        eB, eA = relerr(dev_to_f64(dB), rdB), relerr(dev_to_f64(dA), rdA)
+        assert eB <= TOL["bf16"] and eA <= TOL["bf16"], (call, eB, eA)
+    # the same gradients from the weight half alone (which clears with its own launch)
+    dB2 = torch.full_like(dB, float("nan"))
+    dA2 = torch.full_like(dA, float("nan"))
+    p = ops._problem(X, W, B, ops.BITMAP, s)
+    ws = torch.empty(max(ops.workspace_bytes(W, B, L), 1), dtype=torch.uint8, device="cuda")
+    from paper_2501_08582_amd import _lib
+    st = torch.cuda.current_stream().cuda_stream
+    _lib.check(_lib.backward_weight(p, dY.data_ptr(), X.data_ptr(), M.data_ptr(), B.data_ptr(), A.data_ptr(),
+                                    dB2.data_ptr(), dA2.data_ptr(), None, ws.data_ptr(), ws.numel(), st),
+               "lors_backward_weight")
+    torch.cuda.synchronize()
+    for got, ref in ((dB, dB2), (dA, dA2)):
+        g, f = dev_to_f64(got), dev_to_f64(ref)
+        assert np.linalg.norm(g - f) <= 1e-5 * np.linalg.norm(f)
