@@ -1,12 +1,18 @@
 #!/usr/bin/env python3
 """Throughput of the sparsity-preserved LoRA linear (forward + backward) on one GPU.
 
-One step = lors_forward + lors_backward_data + lors_backward_weight over one
-batch of seeded synthetic inputs already resident in HBM (every step of the
-layer runs in liblors.so; mask packing happens once, before timing).  With
+One step = lors_forward + lors_backward over one batch of seeded synthetic
+inputs already resident in HBM (every step of the layer runs in liblors.so;
+mask preparation -- packing and the transposed layout the backward reads --
+happens once per layer, before timing, since the mask is frozen).  With
 --graph the step is captured once as a HIP graph and replayed (a replay must
 reproduce the eager step first); by default the library calls are issued from
 Python every step.
+
+Before the W warm-up steps the step runs untimed for --settle-s seconds: an
+idle GPU needs on the order of 100 ms of sustained load to reach its working
+clock, so a timed window right after start-up would measure that ramp rather
+than a training loop's steady state.
 
 Prints ONE JSON line: whole-job TFLOP/s over the algorithmic flops
 6RCL + 8rRC per step, the fraction of the bf16 MFMA peak, peak bytes, the
@@ -36,8 +42,10 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-s", type=float, default=1.0,
+                    help="seconds of untimed steps before the warm-up (the GPU leaves its idle clocks)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
@@ -167,6 +175,11 @@ def main():
         print(json.dumps({"pmc_probe": True, "workload": wl.name, "copy_bytes": COPY_BYTES}), flush=True)
         return
 
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < args.settle_s:
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -269,7 +282,8 @@ def main():
                    "sparsity": wl.sparsity, "scale": s,
                    "weight_gradient": "straight-through" if args.ste else "exact masked",
                    "forward_mfma": "structured-sparse" if args.sparse_mfma else "dense",
-                   "step_launch": launch},
+                   "step_launch": launch, "settle_s": args.settle_s,
+                   "mask_prep": "packed mask and its transpose built once per layer, before timing"},
         "pct_mfma_peak": round(100.0 * value / peak, 2),
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),
