@@ -129,10 +129,16 @@ def cpu_baseline(inp, args):
     flops = costs.algorithmic_flops(wl.R, wl.C, Ls, wl.r)
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
                   or [1])
+    cpu_model = next((ln.split(":", 1)[1].strip() for ln in open("/proc/cpuinfo")
+                      if ln.startswith("model name")), "unknown") if os.path.exists("/proc/cpuinfo") else "unknown"
+    blas = next((f"{p.get('internal_api')} {p.get('version')}" for p in threadpool_info()
+                 if p.get("user_api") == "blas"), "unknown")
     return {
         "value": flops / best / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
+        "cpu_model": cpu_model,
+        "blas": f"numpy {np.__version__}, {blas}",
         "kind": "oracle",
         "sample": (f"{wl.name}: {wl.R}x{wl.C} weight, r={wl.r}, {Ls} of {wl.L} tokens; "
                    f"numpy fp64 forward+backward, best of {n} passes ({best:.2f} s each)"),
@@ -247,6 +253,18 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / args.steps
 
+    # Per-step spread: the same step with its own pair of events around each
+    # iteration (markers between steps cost a few microseconds, so the
+    # headline value above comes from the unmarked run).
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    per_step_us = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
+
     avg = {"fwd": per_call(layer.forward),
            "bwd_data": per_call(lambda: layer.backward_data(reuse_mask_t=True)),
            "bwd_weight": per_call(layer.backward_weight)}
@@ -261,10 +279,15 @@ def main():
 
     flops = costs.ste_step_flops(R, C, L, r) if args.ste else costs.algorithmic_flops(R, C, L, r)
     value = flops / (ms_step * 1e-3) / 1e12
+    # executed: every 256-token tile of the forward and dX re-merges its W' tile
+    executed = costs.executed_flops(R, C, L, r, 256, 256)
+    if args.ste:
+        executed += costs.ste_weight_flops(R, C, L, r) - costs.g_flops(R, C, L, r)
     peak = PEAK_TFLOPS[dt]
     dom = max(avg, key=avg.get)
     achieved = kflops[dom] / (avg[dom] * 1e-3) / 1e12
     elt = 2 if dt == "bf16" else 4
+    traffic = measured_traffic(wl.name, kernel_ids[dom])
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -285,6 +308,9 @@ def main():
                    "step_launch": launch, "settle_s": args.settle_s,
                    "mask_prep": "packed mask and its transpose built once per layer, before timing"},
         "pct_mfma_peak": round(100.0 * value / peak, 2),
+        "executed_tflops": round(executed / (ms_step * 1e-3) / 1e12, 2),
+        "step_us_marked": {"median": round(per_step_us[len(per_step_us) // 2], 1),
+                           "min": round(per_step_us[0], 1)},
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),
             "saved_activation": costs.saved_activation_bytes(C, L, elt),
@@ -302,7 +328,8 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": measured_traffic(wl.name, kernel_ids[dom]),
+            "traffic": traffic,
+            "traffic_gbs": round(traffic / (avg[dom] * 1e-3) / 1e9, 1) if traffic else None,
             "algorithmic_bytes": kbytes[dom],
         },
         "wall_s_timed": round(wall, 4),

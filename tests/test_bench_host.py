@@ -70,3 +70,14 @@ def test_cpu_baseline_fields_on_the_small_workload():
     assert out["kind"] == "oracle" and out["unit"] == "TFLOP/s"
     assert out["value"] > 0 and out["cores"] >= 1
     assert "fp32_256x256_r8" in out["sample"]
+    assert out["cpu_model"] and out["blas"].startswith("numpy")
+
+
+def test_executed_flops_count_the_re_merges():
+    from paper_2501_08582_amd import costs
+    R, C, L, r = 4096, 4096, 4096, 16
+    alg = costs.algorithmic_flops(R, C, L, r)
+    ex = costs.executed_flops(R, C, L, r, 256, 256)
+    # 16 token tiles each re-merge W' in the forward and in dX: 15 extra 2rRC per kernel
+    assert ex - alg == 2 * 15 * 2 * r * R * C
+    assert costs.executed_flops(R, C, 256, r, 256, 256) == costs.algorithmic_flops(R, C, 256, r)
