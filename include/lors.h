@@ -130,6 +130,20 @@ typedef enum lors_mask_format {
  * the matrix cores, so it is not faster today. */
 #define LORS_FLAG_FWD_SPARSE_MFMA 0x4u
 
+/* Forward and backward calls: when the forward's or dX's grid of 256 x 256
+ * output tiles ends in a partial wave that fills at most half of the GPU's
+ * compute units (e.g. 320 tiles on 256 CUs), the tiles of that wave are cut
+ * along their contraction (K) into up to 8 pieces, one per CU.  Each piece
+ * writes its fp32 partial sums to the workspace; a small reduction launch
+ * adds a tile's pieces in a fixed order, adds the bias and rounds once to
+ * bf16, so results stay bitwise reproducible.  The workspace grows by the
+ * partials (lors_workspace_bytes accounts for them: at most 64 MiB on a
+ * 256-CU GPU) and lors_forward then requires one too.  No effect for fp32;
+ * applies to ranks up to 64 (above, the layer already runs as two passes).
+ * The weight gradient always splits such a wave: its pieces' partial G tiles
+ * go through the same rank-r products and atomics as whole tiles. */
+#define LORS_FLAG_SPLIT_LAST_WAVE 0x8u
+
 /*
  * Problem description.
  *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
@@ -145,7 +159,8 @@ typedef struct lors_problem {
     float scale;
     int32_t dtype;        /* lors_dtype_t */
     int32_t mask_format;  /* lors_mask_format_t */
-    uint32_t flags;       /* 0 or LORS_FLAG_* bits (REUSE_MASK_T, BWD_STE, FWD_SPARSE_MFMA) */
+    uint32_t flags;       /* 0 or LORS_FLAG_* bits (REUSE_MASK_T, BWD_STE, FWD_SPARSE_MFMA,
+                             SPLIT_LAST_WAVE) */
 } lors_problem_t;
 
 /* Human-readable name of a status code (static storage). */
@@ -199,11 +214,14 @@ lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C
  * 1/16 of W), plus with LORS_FLAG_BWD_STE the P and Q buffers (2*L*rp
  * bytes each, rp = r rounded up to a multiple of 32) and B^T (2*r*R bytes),
  * plus, when r is not a multiple of 8, a copy of B whose rows are padded with
- * zeros to r8 = r rounded up to a multiple of 8 (2*R*r8 bytes), each part
- * rounded up to 256; 0 for fp32.
+ * zeros to r8 = r rounded up to a multiple of 8 (2*R*r8 bytes), plus with
+ * LORS_FLAG_SPLIT_LAST_WAVE the fp32 partial sums of split tiles (forward and
+ * dX; the forward uses only this last part, so a workspace shared by all
+ * calls keeps the transposed mask), each part rounded up to 256; 0 for fp32.
  * (size_t)-1 if p is invalid.  The workspace must be
  * 16-byte aligned, must not overlap any argument, and is overwritten; its
- * contents on return are unspecified.  lors_forward needs no workspace. */
+ * contents on return are unspecified.  lors_forward needs one only with
+ * LORS_FLAG_SPLIT_LAST_WAVE. */
 size_t lors_workspace_bytes(const lors_problem_t* p);
 
 /*

@@ -33,6 +33,7 @@ MASK_2_4 = 1
 FLAG_BWD_STE = 0x1
 FLAG_REUSE_MASK_T = 0x2
 FLAG_FWD_SPARSE_MFMA = 0x4
+FLAG_SPLIT_LAST_WAVE = 0x8
 
 EXPORTED = (
     "lors_status_string", "lors_version", "lors_mask_packed_bytes", "lors_mask_pack",

@@ -50,7 +50,8 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
     if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
     if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
-    if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE | LORS_FLAG_FWD_SPARSE_MFMA)) != 0u)
+    if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE | LORS_FLAG_FWD_SPARSE_MFMA |
+                      LORS_FLAG_SPLIT_LAST_WAVE)) != 0u)
         return LORS_ERR_UNSUPPORTED;
     // the structured-sparse forward exists for bf16 2:4 masks up to rank 64
     if ((p->flags & LORS_FLAG_FWD_SPARSE_MFMA) != 0u &&
@@ -121,10 +122,29 @@ static size_t bpad_bytes(const lors_problem_t* p) {
     if (p->r % 8 == 0) return 0;
     return static_cast<size_t>((2 * p->R * padded_rank(p->r) + 255) / 256 * 256);
 }
+// fp32 partial sums of the forward's or dX's split tiles (the larger of the
+// two; the calls run one after the other), with LORS_FLAG_SPLIT_LAST_WAVE.
+static size_t split_bytes(const lors_problem_t* p) {
+    if ((p->flags & LORS_FLAG_SPLIT_LAST_WAVE) == 0u || p->dtype != LORS_DTYPE_BF16 || p->L == 0) return 0;
+    const int64_t tl = (p->L + 255) / 256;
+    int64_t fwd = 0, dx = 0;
+    if (p->r <= 64 && (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) == 0u)
+        fwd = lors::split_part_bytes(lors::tail_split(tl * ((p->R + 255) / 256), (p->C + 63) / 64));
+    if (padded_rank(p->r) <= 64)
+        dx = lors::split_part_bytes(lors::tail_split(tl * ((p->C + 255) / 256), (p->R + 63) / 64));
+    return static_cast<size_t>(fwd > dx ? fwd : dx);
+}
 size_t lors_workspace_bytes(const lors_problem_t* p) {
     if (p == nullptr || check_problem(p) != LORS_OK) return static_cast<size_t>(-1);
     if (p->dtype != LORS_DTYPE_BF16) return 0;
-    return mt_bytes(p) + ste_bytes(p) + bpad_bytes(p);
+    return mt_bytes(p) + ste_bytes(p) + bpad_bytes(p) + split_bytes(p);
+}
+// The split partials sit after the transposed mask (and the other backward
+// scratch), so a workspace shared by the forward and the backward calls
+// keeps the transposed mask for LORS_FLAG_REUSE_MASK_T.
+static void* split_region(const lors_problem_t* p, void* workspace) {
+    if (workspace == nullptr || split_bytes(p) == 0) return nullptr;
+    return static_cast<uint8_t*>(workspace) + mt_bytes(p) + ste_bytes(p) + bpad_bytes(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -267,8 +287,16 @@ lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W
                          bias ? range_of(bias, R * es) : Range{0, 0}};
     for (const Range& in : ins)
         if (overlap(y, in)) return LORS_ERR_ALIAS;
-    (void)workspace;  // the forward needs no scratch
-    (void)workspace_bytes;
+    // scratch only for the split partial sums (LORS_FLAG_SPLIT_LAST_WAVE)
+    const size_t need = split_bytes(p) ? lors_workspace_bytes(p) : 0;
+    if (need) {
+        if (workspace == nullptr || workspace_bytes < need) return LORS_ERR_WORKSPACE;
+        if (!aligned16(workspace)) return LORS_ERR_ALIGN;
+        const Range w = range_of(workspace, static_cast<int64_t>(need));
+        if (overlap(w, y)) return LORS_ERR_ALIAS;
+        for (const Range& in : ins)
+            if (overlap(w, in)) return LORS_ERR_ALIAS;
+    }
 
     lors::LayerArgs a{};
     a.R = R; a.C = C; a.L = L; a.r = r;
@@ -276,6 +304,7 @@ lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W
     a.two_four = p->mask_format == LORS_MASK_2_4;
     a.sparse_mfma = (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) != 0u;
     a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.bias = bias; a.Y = Y;
+    a.split_ws = need ? split_region(p, workspace) : nullptr;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_fwd_bf16(a, s) : lors::launch_fwd_f32(a, s));
 }
@@ -329,6 +358,7 @@ lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* 
     a.b_pad = (p->dtype == LORS_DTYPE_BF16 && bpad_bytes(p) && workspace)
                   ? static_cast<uint8_t*>(workspace) + mt_bytes(p) + ste_bytes(p)
                   : nullptr;
+    a.split_ws = split_region(p, workspace);
     return a;
 }
 

@@ -75,11 +75,7 @@ __device__ __forceinline__ uint32_t ceil_div_u32(uint32_t a, uint32_t b) {
 // regrouped so that every XCD receives one contiguous range of logical tiles;
 // the logical order then walks `group_m` tile rows at a time, so the tiles an
 // XCD holds at once share few operand panels.
-__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int group_m,
-                                            int& tm, int& tn) {
-    const int total = tiles_m * tiles_n;
-    int t = bid;
-    if ((total & 7) == 0) t = (bid & 7) * (total >> 3) + (bid >> 3);
+__device__ __forceinline__ void group_coords(int t, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
     const int per_group = group_m * tiles_n;
     const int g = t / per_group;
     const int first_m = g * group_m;
@@ -87,6 +83,39 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
     const int within = t - g * per_group;
     tm = first_m + within % gsz;
     tn = within / gsz;
+}
+
+__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int group_m,
+                                            int& tm, int& tn) {
+    const int total = tiles_m * tiles_n;
+    int t = bid;
+    if ((total & 7) == 0) t = (bid & 7) * (total >> 3) + (bid >> 3);
+    group_coords(t, tiles_m, tiles_n, group_m, tm, tn);
+}
+
+// Tile and K-steps of a workgroup when the grid's last, partial wave of tiles
+// is split over K (see tail_split in kernels.hpp).  Ids below n_full take
+// whole tiles -- logical tiles 0 .. n_full-1, regrouped over the XCDs as in
+// tile_coords -- with all nk_all K-steps.  Each remaining logical tile is cut
+// into `split` pieces of consecutive K-steps, one piece per id:
+// piece p covers K-steps [nk_all*p/split, nk_all*(p+1)/split).
+__device__ __forceinline__ void work_coords(int bid, int tiles_m, int tiles_n, int group_m, int n_full,
+                                            int split, int64_t nk_all, int& tm, int& tn, int64_t& kbeg,
+                                            int64_t& nk) {
+    int t;
+    if (bid < n_full) {
+        t = bid;
+        if ((n_full & 7) == 0) t = (bid & 7) * (n_full >> 3) + (bid >> 3);
+        kbeg = 0;
+        nk = nk_all;
+    } else {
+        const int j = bid - n_full;
+        const int q = j / split, p = j - q * split;
+        t = n_full + q;
+        kbeg = nk_all * p / split;
+        nk = nk_all * (p + 1) / split - kbeg;
+    }
+    group_coords(t, tiles_m, tiles_n, group_m, tm, tn);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }

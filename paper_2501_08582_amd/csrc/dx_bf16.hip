@@ -67,7 +67,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
     int ra, float s, int tiles_m, int tiles_n, int ldb, float* __restrict__ z0, int64_t nz0,
-    float* __restrict__ z1, int64_t nz1) {
+    float* __restrict__ z1, int64_t nz1, int n_full, int split, float* __restrict__ part) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -91,11 +91,15 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         }
     }
 
+    // tile and K-steps: ids past n_full are pieces of split tiles (their
+    // partial sums go to `part`, see the epilogue)
     int tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, tm, tn);
+    int64_t kbeg64, nk64;
+    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (R + BK - 1) / BK, tm, tn, kbeg64, nk64);
     const int64_t m0 = (int64_t)tm * BM;
     const int n0 = tn * BN;
-    const int nk = (R + BK - 1) / BK;
+    const int nk = (int)nk64;
+    const int kofs = (int)kbeg64 * BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
@@ -158,6 +162,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint32_t* Mn = uniform_ptr(Mt + (int64_t)n0 * wprT);
 
     auto copy_j = [&](int j, int k0, uint32_t sb) {
+        k0 += kofs;
         if (j < 8) {
             const int q = j, blk = 8 * wave + q;
             const uint32_t dst = sb + Lay::D + 1024 * blk;
@@ -355,6 +360,20 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     // (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
+    if ((int)blockIdx.x >= n_full) {
+        // a piece of a split tile: its unrounded fp32 partial sums go to slice
+        // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
+        // reduction launch adds the pieces in order and rounds once
+        float* dst = part + (int64_t)((int)blockIdx.x - n_full) * (BM * BN);
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + ncol0 + 32 * nb] = acc[mb][nb][v];
+        return;
+    }
     uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
@@ -382,7 +401,12 @@ template <int RK, bool PASS2>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool clear) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
-    dim3 grid(tiles_m * tiles_n), block(NT);
+    // a partial last wave of tiles is cut over K when the caller gave room
+    // for the pieces' partial sums (one pass only: ranks up to 64)
+    TailSplit sp{tiles_m * tiles_n, 1, tiles_m * tiles_n};
+    if (a.split_ws != nullptr && !PASS2 && ldb <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.R + BK - 1) / BK);
+    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
+    dim3 grid(sp.grid), block(NT);
     // fixed-offset copies: whole tiles and K-steps, and per-lane byte
     // offsets (256 dY rows of R, 64 W rows of C, 256 M^T rows) inside 32 bits
     const int64_t wprT = (a.R + 31) / 32;
@@ -400,11 +424,17 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool c
     const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
     if (ragged)
         hipLaunchKernelGGL((dx_kernel<RK, true, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1);
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, sp.n_full,
+                           sp.split, part);
     else
         hipLaunchKernelGGL((dx_kernel<RK, false, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1);
-    return hipGetLastError();
+                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, sp.n_full,
+                           sp.split, part);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && sp.split > 1)
+        e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.C, nullptr,
+                                     dX, st);
+    return e;
 }
 
 // a.r: the (padded) rank of this pass; ra: the rows of A that exist

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, const uint16_t* __restrict__ bias,
     uint16_t* __restrict__ Y, int64_t L, int R, int C, int r, float s, int tiles_m,
-    int tiles_n, int ldb) {
+    int tiles_n, int ldb, int n_full, int split, float* __restrict__ part) {
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
@@ -86,11 +86,15 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
+    // tile and K-steps: ids past n_full are pieces of split tiles (their
+    // partial sums go to `part`, see the epilogue)
     int tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, tm, tn);
+    int64_t kbeg64, nk64;
+    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg64, nk64);
     const int64_t m0 = (int64_t)tm * BM;
     const int n0 = tn * BN;
-    const int nk = (C + BK - 1) / BK;
+    const int nk = (int)nk64;
+    const int kofs = (int)kbeg64 * BK;
     const int wpr = (C + 31) >> 5;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * (lane & 7);
@@ -154,6 +158,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 
     // copy j of the stage at K offset k0 into the stage at LDS address sb
     auto copy_j = [&](int j, int k0, uint32_t sb) {
+        k0 += kofs;
         if (j < 16) {
             const int q = j & 7;
             const bool isx = j < 8;
@@ -351,6 +356,20 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // LDS (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
+    if ((int)blockIdx.x >= n_full) {
+        // a piece of a split tile: its unrounded fp32 partial sums go to slice
+        // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
+        // reduction launch adds the pieces in order, adds the bias and rounds
+        float* dst = part + (int64_t)((int)blockIdx.x - n_full) * (BM * BN);
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + nrow0 + 32 * nb] = acc[mb][nb][v];
+        return;
+    }
     uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -381,7 +400,12 @@ template <int RK, bool TWO_FOUR, bool PASS2>
 hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.R + BN - 1) / BN);
-    dim3 grid(tiles_m * tiles_n), block(NT);
+    // a partial last wave of tiles is cut over K when the caller gave room
+    // for the pieces' partial sums (one pass only: ranks up to 64)
+    TailSplit sp{tiles_m * tiles_n, 1, tiles_m * tiles_n};
+    if (a.split_ws != nullptr && !PASS2 && a.r <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.C + BK - 1) / BK);
+    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
+    dim3 grid(sp.grid), block(NT);
     auto* X = (const uint16_t*)a.X;
     auto* W = (const uint16_t*)a.W;
     auto* B = (const uint16_t*)a.B;
@@ -394,11 +418,16 @@ hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     const bool ragged = a.L % BM != 0 || a.R % BN != 0 || a.C % BK != 0 || (int64_t)BM * a.C * 2 >= (1ll << 31);
     if (ragged)
         hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
+                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
+                           part);
     else
         hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb);
-    return hipGetLastError();
+                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
+                           part);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && sp.split > 1)
+        e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.R, bias, Y, st);
+    return e;
 }
 
 template <int RK>

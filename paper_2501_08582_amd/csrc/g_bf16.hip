@@ -54,7 +54,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, float* __restrict__ dB, float* __restrict__ dA,
-    int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n) {
+    int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n, int n_full, int split) {
     constexpr int JB = (RK + 1) / 2;  // 32-wide blocks of the rank
     static_assert(GT_BYTES <= SMEM, "G^T tile fits");
     static_assert(EP_B + BM * 32 * JB * 2 <= EP_X && EP_X + 2 * 16 * kWave * 4 <= SMEM, "B block and dA exchange fit");
@@ -67,11 +67,16 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const int h = lane >> 5;
     const int wi = wave >> 1, wj = wave & 1;
 
+    // tile and token range: a piece of a split tile covers K-steps
+    // [kbeg, kbeg + nk); its G is a partial sum over those tokens, and since
+    // the mask select and both rank-r products are linear in G, the pieces'
+    // contributions add up in dB and dA like those of different tiles
     int tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, tm, tn);
+    int64_t kbeg, nk;
+    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (L + BK - 1) / BK, tm, tn, kbeg, nk);
     const int i0 = tm * BM;
     const int j0 = tn * BN;
-    const int64_t nk = (L + BK - 1) / BK;
+    const int64_t kofs = kbeg * BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
 
     // ---- asynchronous slab copies: copy pair q of this wave fills tile row
@@ -92,6 +97,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint16_t* dYt = uniform_ptr(dY + i0);
     const uint16_t* Xt = uniform_ptr(X + j0);
     auto copy_pair = [&](int q, int64_t k0, uint32_t sb) {
+        k0 += kofs;
         const uint32_t da = sb + (LOADS * wave + q) * 1024, xa = da + TILEB;
         if constexpr (!RAGGED) {
             copy16s_to_lds(uniform_ptr(dYt + k0 * R), offD[q], da);
@@ -400,7 +406,8 @@ template <int RK>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     const int tiles_m = (int)((a.R + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
-    dim3 grid(tiles_m * tiles_n), block(NT);
+    const TailSplit sp = tail_split((int64_t)tiles_m * tiles_n, (a.L + BK - 1) / BK);
+    dim3 grid(sp.grid), block(NT);
     auto* dY = (const uint16_t*)a.dY;
     auto* X = (const uint16_t*)a.X;
     auto* B = (const uint16_t*)a.B;
@@ -411,10 +418,10 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
                         (int64_t)BK * a.R * 2 >= (1ll << 31) || (int64_t)BK * a.C * 2 >= (1ll << 31);
     if (ragged)
         hipLaunchKernelGGL((g_kernel<RK, true>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, sp.n_full, sp.split);
     else
         hipLaunchKernelGGL((g_kernel<RK, false>), grid, block, 0, st, dY, X, a.Mt, B, A, a.dB, a.dA, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n);
+                           (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, sp.n_full, sp.split);
     return hipGetLastError();
 }
 

@@ -31,7 +31,29 @@ struct LayerArgs {
     void* b_pad;            // R x roundup8(r) scratch for B when r % 8 != 0 (bf16 backward), else nullptr
     bool clear_grads;       // the bf16 dX launch also clears dB and dA (combined backward)
     int64_t r_grad;         // rank of dB and dA (the caller's r; the dX passes change a.r)
+    void* split_ws;         // fp32 partial sums of split tiles (forward, dX), or nullptr: no split
 };
+
+// Split of a grid of `tiles` output tiles whose K-loop has nk steps.  Whole
+// waves of tiles (one per CU) run unsplit; a last, partial wave that fills at
+// most half of the CUs is cut over K into `split` pieces per tile -- as many
+// as fill the CUs, at most 8, each at least 4 K-steps -- so that it does not
+// leave most of the chip idle.  n_full: the tiles that run whole; the grid
+// has n_full + (tiles - n_full) * split workgroups.
+struct TailSplit {
+    int n_full, split, grid;
+};
+TailSplit tail_split(int64_t tiles, int64_t nk);
+// Bytes of fp32 partial sums a split grid of 256 x 256 tiles writes.
+inline int64_t split_part_bytes(const TailSplit& t) {
+    return t.split > 1 ? (int64_t)(t.grid - t.n_full) * 256 * 256 * 4 : 0;
+}
+// out (rows x cols, bf16) on the split tiles = the sum of their pieces'
+// partials in piece order (+ bias[col] when bias is not null), rounded once.
+// Tile coordinates follow work_coords with the same tiles_m, tiles_n, group_m.
+hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, int tiles_m, int tiles_n,
+                                    int group_m, int64_t rows, int cols, const void* bias, void* out,
+                                    hipStream_t s);
 
 // bf16 path
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);

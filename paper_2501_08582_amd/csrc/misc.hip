@@ -270,6 +270,67 @@ hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t st) {
     return hipGetLastError();
 }
 
+// Workgroup (q, rb): rows 4*rb .. 4*rb+3 of split tile q (logical tile
+// n_full + q); thread t covers 4 columns of one of those rows.
+__global__ __launch_bounds__(NT) void split_reduce_kernel(const float* __restrict__ part, int n_full, int split,
+                                                          int tiles_m, int tiles_n, int group_m, int64_t rows,
+                                                          int cols, const uint16_t* __restrict__ bias,
+                                                          uint16_t* __restrict__ out) {
+    const int q = blockIdx.x >> 6, rb = blockIdx.x & 63;
+    int tm, tn;
+    group_coords(n_full + q, tiles_m, tiles_n, group_m, tm, tn);
+    const int tr = 4 * rb + (threadIdx.x >> 6), tc = 4 * (threadIdx.x & 63);
+    const int64_t gm = (int64_t)tm * 256 + tr;
+    const int gn = tn * 256 + tc;
+    if (gm >= rows || gn >= cols) return;
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < split; ++p)
+        sum += *(const f32x4*)(part + ((int64_t)q * split + p) * 65536 + tr * 256 + tc);
+    uint16_t* o = out + gm * cols + gn;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        if (gn + e < cols) {
+            const float b = bias != nullptr ? bf16_bits_to_f32(bias[gn + e]) : 0.f;
+            o[e] = bf16_bits(sum[e] + b);
+        }
+    }
+}
+
+hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, int tiles_m, int tiles_n,
+                                    int group_m, int64_t rows, int cols, const void* bias, void* out,
+                                    hipStream_t st) {
+    const int tail = tiles_m * tiles_n - n_full;
+    if (tail <= 0 || split < 2) return hipSuccess;
+    hipLaunchKernelGGL(split_reduce_kernel, dim3(tail * 64), dim3(NT), 0, st, part, n_full, split, tiles_m, tiles_n,
+                       group_m, rows, cols, (const uint16_t*)bias, (uint16_t*)out);
+    return hipGetLastError();
+}
+
+TailSplit tail_split(int64_t tiles, int64_t nk) {
+    // compute units of the current device, read once per device
+    static int cus_of[64];
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+        if (cus_of[dev] == 0) {
+            int n = 0;
+            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+                cus_of[dev] = n;
+        }
+        if (cus_of[dev] > 0) cus = cus_of[dev];
+    }
+    TailSplit t{(int)tiles, 1, (int)tiles};
+    const int64_t tail = tiles % cus;
+    if (tail == 0 || 2 * tail > cus) return t;
+    int64_t s = cus / tail;
+    if (s > 8) s = 8;
+    if (s > nk / 4) s = nk / 4;
+    if (s < 2) return t;
+    t.n_full = (int)(tiles - tail);
+    t.split = (int)s;
+    t.grid = (int)(t.n_full + tail * s);
+    return t;
+}
+
 hipError_t launch_zero2_f32(float* a, int64_t na, float* b, int64_t nb, hipStream_t st) {
     const int64_t n = na + nb;
     if (n == 0) return hipSuccess;

@@ -119,20 +119,26 @@ def _problem(X2, W, B, mask_format, scale, L=None, flags=0):
 
 def forward(X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor, A: torch.Tensor,
             scale: float, mask_format=BITMAP, bias: Optional[torch.Tensor] = None,
-            out: Optional[torch.Tensor] = None, sparse_mfma: bool = False) -> torch.Tensor:
+            out: Optional[torch.Tensor] = None, sparse_mfma: bool = False,
+            split_last_wave: bool = False) -> torch.Tensor:
     """Y = X . select(M, W + scale.B.A, 0)^T (+ bias).  X may have leading dims.
     ``sparse_mfma`` (2:4 masks, bf16, r <= 64) multiplies on the structured-
-    sparse MFMA instead of the dense one."""
+    sparse MFMA instead of the dense one.  ``split_last_wave`` cuts a partial
+    last wave of output tiles over K (LORS_FLAG_SPLIT_LAST_WAVE; a workspace
+    is allocated here)."""
     lead = X.shape[:-1]
     X2 = X.reshape(-1, X.shape[-1])
     dev = _dev(X2, W, M, B, A, bias)
     R = W.shape[0]
     if out is None:
         out = torch.empty((X2.shape[0], R), dtype=W.dtype, device=dev)
-    p = _problem(X2, W, B, mask_format, scale, flags=_lib.FLAG_FWD_SPARSE_MFMA if sparse_mfma else 0)
+    flags = (_lib.FLAG_FWD_SPARSE_MFMA if sparse_mfma else 0) | (_lib.FLAG_SPLIT_LAST_WAVE if split_last_wave else 0)
+    p = _problem(X2, W, B, mask_format, scale, flags=flags)
+    need = _lib.workspace_bytes(p) if split_last_wave else 0
+    ws = torch.empty(need, dtype=torch.uint8, device=dev) if need else None
     with torch.cuda.device(dev):
         _lib.check(_lib.forward(p, _ptr(X2), _ptr(W), _ptr(M), _ptr(B), _ptr(A), _ptr(bias), _ptr(out),
-                                None, 0, _stream(dev)), "lors_forward")
+                                _ptr(ws), need, _stream(dev)), "lors_forward")
     return out.view(*lead, R)
 
 
@@ -150,14 +156,15 @@ def workspace_bytes(W: torch.Tensor, B: torch.Tensor, L: int, mask_format=BITMAP
 def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor, B: torch.Tensor,
              A: torch.Tensor, scale: float, mask_format=BITMAP, need_dx: bool = True,
              need_dbias: bool = False, out: Optional[Tuple] = None,
-             workspace: Optional[torch.Tensor] = None, ste: bool = False):
+             workspace: Optional[torch.Tensor] = None, ste: bool = False, split_last_wave: bool = False):
     """(dX, dB, dA, dbias); dB/dA/dbias are fp32.
 
     By default dB, dA are the exact, masked gradient.  ``ste=True`` gives the
     straight-through, re-associated adapter gradients of Section 2.3 (bf16
-    only); dX is the same either way.  ``workspace`` (uint8, at least
-    :func:`workspace_bytes` with the same ``ste``) is allocated here when not
-    given."""
+    only); dX is the same either way.  ``split_last_wave`` cuts a partial
+    last wave of dX tiles over K (LORS_FLAG_SPLIT_LAST_WAVE).  ``workspace``
+    (uint8, at least what the library reports for the same flags) is
+    allocated here when not given."""
     X2 = X.reshape(-1, X.shape[-1])
     dY2 = dY.reshape(-1, dY.shape[-1])
     dev = _dev(dY2, X2, W, M, B, A)
@@ -171,7 +178,8 @@ def backward(dY: torch.Tensor, X: torch.Tensor, W: torch.Tensor, M: torch.Tensor
         dB = torch.empty((R, r), dtype=torch.float32, device=dev)
         dA = torch.empty((r, C), dtype=torch.float32, device=dev)
         dbias = torch.empty(R, dtype=torch.float32, device=dev) if need_dbias else None
-    p = _problem(X2, W, B, mask_format, scale, flags=_lib.FLAG_BWD_STE if ste else 0)
+    flags = (_lib.FLAG_BWD_STE if ste else 0) | (_lib.FLAG_SPLIT_LAST_WAVE if split_last_wave else 0)
+    p = _problem(X2, W, B, mask_format, scale, flags=flags)
     need = _lib.workspace_bytes(p)
     if workspace is None and need:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)

@@ -62,14 +62,17 @@ class LayerStep:
         self.dA = torch.empty((r, C), dtype=torch.float32, device="cuda")
         ldt = _lib.DTYPE_BF16 if dt == "bf16" else _lib.DTYPE_F32
         lfmt = _lib.MASK_2_4 if self.fmt == ops.TWO_FOUR else _lib.MASK_BITMAP
-        self.p = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt)
-        self.p_fwd = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_FWD_SPARSE_MFMA) if sparse_mfma
+        # every call splits a partial last wave of output tiles over K
+        sp = _lib.FLAG_SPLIT_LAST_WAVE
+        self.p = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, sp)
+        self.p_fwd = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, sp | _lib.FLAG_FWD_SPARSE_MFMA) if sparse_mfma
                       else self.p)
-        self.p_reuse = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_REUSE_MASK_T)
-        self.p_weight = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, _lib.FLAG_BWD_STE) if ste else self.p_reuse)
+        self.p_reuse = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt, sp | _lib.FLAG_REUSE_MASK_T)
+        self.p_weight = (_lib.problem(R, C, L, r, wl.scale, ldt, lfmt, sp | _lib.FLAG_BWD_STE) if ste
+                         else self.p_reuse)
         self.p_bwd = _lib.problem(R, C, L, r, wl.scale, ldt, lfmt,
-                                  _lib.FLAG_REUSE_MASK_T | (_lib.FLAG_BWD_STE if ste else 0))
-        self.ws = max(_lib.workspace_bytes(self.p), _lib.workspace_bytes(self.p_weight))
+                                  sp | _lib.FLAG_REUSE_MASK_T | (_lib.FLAG_BWD_STE if ste else 0))
+        self.ws = max(_lib.workspace_bytes(q) for q in (self.p, self.p_fwd, self.p_weight, self.p_bwd))
         self.wsbuf = torch.empty(max(self.ws, 1), dtype=torch.uint8, device="cuda")
         # mask preparation, once per layer: the transposed mask into the workspace
         self.backward_data()
@@ -81,7 +84,8 @@ class LayerStep:
     def forward(self) -> None:
         _, sh = self._ptrs()
         _lib.check(_lib.forward(self.p_fwd, self.X.data_ptr(), self.W.data_ptr(), self.M.data_ptr(), self.B.data_ptr(),
-                                self.A.data_ptr(), None, self.Y.data_ptr(), None, 0, sh), "lors_forward")
+                                self.A.data_ptr(), None, self.Y.data_ptr(), self.wsbuf.data_ptr(), self.ws, sh),
+                   "lors_forward")
 
     def backward_data(self, reuse_mask_t: bool = False) -> None:
         """dX; builds the transposed mask in the workspace unless told it is

@@ -178,7 +178,7 @@ def test_shape(lib, kw):
 
 
 @pytest.mark.parametrize("kw", [dict(R=60), dict(C=36), dict(dtype=_lib.DTYPE_F32, C=66),
-                                dict(flags=0x8), dict(dtype=_lib.DTYPE_F32, flags=_lib.FLAG_BWD_STE),
+                                dict(flags=0x10), dict(dtype=_lib.DTYPE_F32, flags=_lib.FLAG_BWD_STE),
                                 # the structured-sparse forward: bf16 2:4 masks up to rank 64 only
                                 dict(flags=_lib.FLAG_FWD_SPARSE_MFMA),
                                 dict(mask_format=_lib.MASK_2_4, dtype=_lib.DTYPE_F32, flags=_lib.FLAG_FWD_SPARSE_MFMA),
@@ -292,3 +292,44 @@ def test_no_weak_symbol_defined_twice():
     if not all(os.path.exists(o) for o in objs):
         pytest.skip("library objects not built")
     pbuild._check_no_shared_weak_symbols(objs)
+
+
+def _tail_split_bytes(tiles, nk, cus=256):
+    """Partials of a split grid: a last, partial wave of at most half the CUs
+    is cut into min(8, cus // tail, nk // 4) pieces per tile (when >= 2)."""
+    tail = tiles % cus
+    if tail == 0 or 2 * tail > cus:
+        return 0
+    s = min(8, cus // tail, nk // 4)
+    return tail * s * 256 * 256 * 4 if s >= 2 else 0
+
+
+def test_workspace_query_split_last_wave(lib):
+    F = _lib.FLAG_SPLIT_LAST_WAVE
+    for R, C, L, r in [(5120, 5120, 4096, 64), (4096, 1024, 4352, 16), (4104, 1000, 4300, 5), (4096, 4096, 4096, 16),
+                       (256, 256, 256, 8), (4096, 1024, 4352, 100), (13824, 5120, 4096, 64)]:
+        base = _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r))
+        tl = -(-L // 256)
+        fwd = _tail_split_bytes(tl * -(-R // 256), -(-C // 64)) if r <= 64 else 0
+        dx = _tail_split_bytes(tl * -(-C // 256), -(-R // 64)) if -(-r // 8) * 8 <= 64 else 0
+        assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=F)) == base + max(fwd, dx), (R, C, L, r)
+    # 5120 x 5120 at 4096 tokens: 320 tiles, 64 in 4 pieces each, 64 MiB of partials
+    assert _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64, flags=F)) - \
+        _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64)) == 64 << 20
+    # no effect for fp32, and none without tokens
+    assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32, flags=F)) == 0
+    assert _lib.workspace_bytes(_p(L=0, flags=F)) == _lib.workspace_bytes(_p(L=0))
+
+
+def test_forward_requires_workspace_with_split_flag(lib):
+    # validation happens before any HIP call, so this runs without a GPU
+    p = _p(R=4096, C=1024, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
+    need = _lib.workspace_bytes(p)
+    assert need > 0
+    fake = 1 << 40  # 16-byte aligned, never dereferenced
+    args = [fake + i * (1 << 32) for i in range(6)]
+    st = _lib.forward(p, args[0], args[1], args[2], args[3], args[4], None, args[5], None, 0, None)
+    assert st == _lib.ERR_WORKSPACE
+    st = _lib.forward(p, args[0], args[1], args[2], args[3], args[4], None, args[5], fake + 7 * (1 << 32), need - 1,
+                      None)
+    assert st == _lib.ERR_WORKSPACE

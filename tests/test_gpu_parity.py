@@ -532,3 +532,55 @@ def test_combined_backward_overwrites_gradients(R, C, L, r):
     for got, ref in ((dB, dB2), (dA, dA2)):
         g, f = dev_to_f64(got), dev_to_f64(ref)
         assert np.linalg.norm(g - f) <= 1e-5 * np.linalg.norm(f)
+
+
+# ---------------------------------------------------------------------------
+# grids with a partial last wave: the weight-gradient kernel cuts each tile
+# of that wave over the tokens (K) and adds the pieces' contributions with
+# its atomics.  8448 x 2304 is 33 x 9 = 297 tiles: 256 whole, 41 in pieces.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,L,r,mask", [(8448, 2304, 1024, 16, "magnitude"), (8408, 2304, 1000, 64, "2:4"),
+                                          (8448, 2304, 512, 5, "magnitude")])
+def test_weight_gradient_tail_split(R, C, L, r, mask):
+    inp = _inputs("llama2_7b_q_proj", R=R, C=C, r=r, mask=mask, seed=1300 + r, L=L)
+    _check_all(inp)
+
+
+# ---------------------------------------------------------------------------
+# LORS_FLAG_SPLIT_LAST_WAVE: forward and dX tiles of a partial last wave cut
+# over K, fp32 partials reduced in a fixed order.  4352 tokens x 4096 outputs
+# is 17 x 16 = 272 forward tiles (256 whole, 16 in pieces); dX over 1024
+# inputs is 68 tiles, all in pieces; the weight gradient's 64 tiles too.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,L,r,mask,bias", [(4096, 1024, 4352, 16, "magnitude", False),
+                                               (4104, 1000, 4300, 5, "magnitude", True),
+                                               (4096, 1024, 4352, 64, "2:4", False),
+                                               (4096, 1024, 4352, 100, "magnitude", False)])
+def test_split_last_wave(R, C, L, r, mask, bias):
+    inp = _inputs("llama2_7b_q_proj", R=R, C=C, r=r, mask=mask, seed=1500 + r, L=L)
+    dt = "bf16"
+    X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    fmt = FMT[mask]
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
+    s = inp.wl.scale
+    bias_bits = (synth.f32_to_bf16_bits(np.random.default_rng(7).standard_normal(R).astype(np.float32) * 0.1)
+                 if bias else None)
+    bias_t = to_dev(bias_bits, dt) if bias else None
+    print("split last wave", (R, C, L, r, mask, bias), flush=True)
+    Y = ops.forward(X, W, M, B, A, s, fmt, bias=bias_t, split_last_wave=True)
+    dX, dB, dA, _ = ops.backward(dY, X, W, M, B, A, s, fmt, split_last_wave=True)
+    Y0 = ops.forward(X, W, M, B, A, s, fmt, bias=bias_t)
+    dX0, _, _, _ = ops.backward(dY, X, W, M, B, A, s, fmt)
+    # deterministic: a second split call gives the same bits
+    Y1 = ops.forward(X, W, M, B, A, s, fmt, bias=bias_t, split_last_wave=True)
+    dX1, _, _, _ = ops.backward(dY, X, W, M, B, A, s, fmt, split_last_wave=True)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y1) and torch.equal(dX, dX1)
+    rY, rdX, rdB, rdA, _ = oracle_full(inp, s, to_f64(bias_bits, dt) if bias else None)
+    errs = {"Y": relerr(dev_to_f64(Y), rY), "dX": relerr(dev_to_f64(dX), rdX),
+            "dB": relerr(dev_to_f64(dB), rdB), "dA": relerr(dev_to_f64(dA), rdA),
+            "Y vs unsplit": relerr(dev_to_f64(Y), dev_to_f64(Y0)),
+            "dX vs unsplit": relerr(dev_to_f64(dX), dev_to_f64(dX0))}
+    print(errs, flush=True)
+    for k, e in errs.items():
+        assert e <= TOL[dt], f"{k}: rel err {e:.3e}"
