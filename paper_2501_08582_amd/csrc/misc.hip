@@ -1,5 +1,6 @@
 // Mask packing (dense 0/1 or weight != 0 -> 1 bit per element), unpacking,
-// output clearing and the bias gradient.
+// output clearing, the bias gradient, and the split of a short last wave of
+// tiles over K (the rule and the reduction of the pieces' partial sums).
 //
 // Packed layouts (the paper keeps the mask as a dense boolean; the packing is
 // this library's own):
@@ -7,6 +8,8 @@
 //   2:4:    group g of row i keeps p0 < p1; nibble p0 | p1 << 2 at bits
 //           4*(g % 8) of word i*ceil(C/32) + g/8
 // One thread produces one packed word from 32 consecutive elements of a row.
+#include <atomic>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -307,16 +310,15 @@ hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, in
 }
 
 TailSplit tail_split(int64_t tiles, int64_t nk) {
-    // compute units of the current device, read once per device
-    static int cus_of[64];
+    // compute units of the current device, read once per device (calls from
+    // several host threads may both read it; they store the same value)
+    static std::atomic<int> cus_of[64];
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
-        if (cus_of[dev] == 0) {
-            int n = 0;
-            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-                cus_of[dev] = n;
-        }
-        if (cus_of[dev] > 0) cus = cus_of[dev];
+        int n = cus_of[dev].load(std::memory_order_relaxed);
+        if (n == 0 && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+            cus_of[dev].store(n, std::memory_order_relaxed);
+        if (n > 0) cus = n;
     }
     TailSplit t{(int)tiles, 1, (int)tiles};
     const int64_t tail = tiles % cus;
