@@ -99,9 +99,10 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
 // tile_coords -- with all nk_all K-steps.  Each remaining logical tile is cut
 // into `split` pieces of consecutive K-steps, one piece per id:
 // piece p covers K-steps [nk_all*p/split, nk_all*(p+1)/split).
+// (K-step counts fit 32 bits: every extent is below 2^31 and a K-step spans
+// 64 elements.)
 __device__ __forceinline__ void work_coords(int bid, int tiles_m, int tiles_n, int group_m, int n_full,
-                                            int split, int64_t nk_all, int& tm, int& tn, int64_t& kbeg,
-                                            int64_t& nk) {
+                                            int split, int nk_all, int& tm, int& tn, int& kbeg, int& nk) {
     int t;
     if (bid < n_full) {
         t = bid;

@@ -89,12 +89,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // tile and K-steps: ids past n_full are pieces of split tiles (their
     // partial sums go to `part`, see the epilogue)
     int tm, tn;
-    int64_t kbeg64, nk64;
-    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg64, nk64);
+    int kbeg, nk;
+    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg, nk);
     const int64_t m0 = (int64_t)tm * BM;
     const int n0 = tn * BN;
-    const int nk = (int)nk64;
-    const int kofs = (int)kbeg64 * BK;
+    const int kofs = kbeg * BK;
     const int wpr = (C + 31) >> 5;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * (lane & 7);

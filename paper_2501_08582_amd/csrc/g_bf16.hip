@@ -72,11 +72,12 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     // the mask select and both rank-r products are linear in G, the pieces'
     // contributions add up in dB and dA like those of different tiles
     int tm, tn;
-    int64_t kbeg, nk;
-    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (L + BK - 1) / BK, tm, tn, kbeg, nk);
+    int kbeg, nk32;
+    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (int)((L + BK - 1) / BK), tm, tn, kbeg, nk32);
+    const int64_t nk = nk32;
     const int i0 = tm * BM;
     const int j0 = tn * BN;
-    const int64_t kofs = kbeg * BK;
+    const int64_t kofs = (int64_t)kbeg * BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
 
     // ---- asynchronous slab copies: copy pair q of this wave fills tile row
