@@ -101,10 +101,18 @@ def draw_inputs(R: int, C: int, L: int, r: int, mask: str, seed: int):
     return X, W, B, A, dY, M
 
 
-def _time(fn, steps: int, warmup: int) -> float:
+def _time(fn, steps: int, warmup: int, settle_s: float = 0.25) -> float:
+    """Mean HIP-event time of `fn` over `steps` calls, after `warmup` calls
+    and at least `settle_s` seconds of untimed calls (an idle GPU takes on
+    the order of 100 ms of load to reach its working clock)."""
     st = torch.cuda.current_stream()
-    for _ in range(warmup):
+    t0 = time.perf_counter()
+    n = 0
+    while n < warmup or time.perf_counter() - t0 < settle_s:
         fn()
+        n += 1
+        if n % 10 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record(st)
