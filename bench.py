@@ -17,7 +17,12 @@ than a training loop's steady state.
 Prints ONE JSON line: whole-job TFLOP/s over the algorithmic flops
 6RCL + 8rRC per step, the fraction of the bf16 MFMA peak, peak bytes, the
 roofline entry of the dominant kernel (HIP-event durations on the launch
-stream) and the fp64 CPU oracle timed on the host's cores.
+stream) and the fp64 CPU oracle timed on the host's cores.  The default
+workload is the largest single-GPU projection, Llama-3-8B down_proj
+(4096 x 14336, 8192 tokens, r = 64, 70 % magnitude mask); the two
+Llama-2-7B projections (q_proj 4096 x 4096; up_proj 11008 x 4096 with a 2:4
+mask) are timed in the same run and reported under "other_workloads"
+(--also '' turns that off).
 """
 from __future__ import annotations
 
@@ -32,7 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "masked-LoRA linear fwd+bwd TFLOP/s (bf16) and % of MFMA peak; peak bytes"
-DEFAULT_WORKLOAD = "llama2_7b_q_proj"
+DEFAULT_WORKLOAD = "llama3_8b_down_proj"
+DEFAULT_ALSO = "llama2_7b_q_proj,llama2_7b_up_proj_2_4"
 # MI355X dense MFMA peaks in TFLOP/s: 256 CUs x 4 matrix cores x 2.4 GHz x
 # (1024 bf16 or 256 fp32 flops per clock per matrix core).  HBM3E 8 TB/s.
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
@@ -47,6 +53,9 @@ def parse():
     ap.add_argument("--settle-s", type=float, default=1.0,
                     help="seconds of untimed steps before the warm-up (the GPU leaves its idle clocks)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--also", default=DEFAULT_ALSO,
+                    help="comma-separated workloads whose step is also timed (same settling, warm-up and step "
+                         "count) and reported under other_workloads; '' for none")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -334,9 +343,49 @@ def main():
         },
         "wall_s_timed": round(wall, 4),
     }
+    others = [w for w in args.also.split(",") if w and w != wl.name] if not (args.graph or args.pmc_probe) else []
+    if others:
+        del layer
+        torch.cuda.empty_cache()
+        out["other_workloads"] = [time_other(w, args) for w in others]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp, args)
     print(json.dumps(out), flush=True)
+
+
+def time_other(name, args):
+    """Step time of another workload, measured like the headline (settling,
+    warm-up, K steps between two events on the launch stream)."""
+    import torch
+
+    from paper_2501_08582_amd import costs, synth
+    from paper_2501_08582_amd.step import LayerStep
+
+    wl = synth.workload(name)
+    layer = LayerStep(synth.make(wl), ste=args.ste, sparse_mfma=args.sparse_mfma)
+    stream = torch.cuda.current_stream()
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < args.settle_s:
+        for _ in range(20):
+            layer.run()
+        torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        layer.run()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        layer.run()
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    R, C, L, r = wl.R, wl.C, wl.L, wl.r
+    flops = costs.ste_step_flops(R, C, L, r) if args.ste else costs.algorithmic_flops(R, C, L, r)
+    tf = flops / (ms * 1e-3) / 1e12
+    del layer
+    torch.cuda.empty_cache()
+    return {"workload": name, "R": R, "C": C, "L": L, "r": r, "mask": wl.mask, "ms_per_step": round(ms, 4),
+            "tflops": round(tf, 2), "pct_mfma_peak": round(100.0 * tf / PEAK_TFLOPS[wl.dtype], 2)}
 
 
 if __name__ == "__main__":

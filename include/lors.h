@@ -134,20 +134,27 @@ typedef enum lors_mask_format {
  * output tiles ends in a partial wave that fills at most half of the GPU's
  * compute units (e.g. 320 tiles on 256 CUs), the tiles of that wave are cut
  * along their contraction (K) into up to 8 pieces, one per CU.  Each piece
- * writes its fp32 partial sums to the workspace; a small reduction launch
- * adds a tile's pieces in a fixed order, adds the bias and rounds once to
- * bf16, so results stay bitwise reproducible.  The workspace grows by the
- * partials (lors_workspace_bytes accounts for them: at most 64 MiB on a
- * 256-CU GPU) and lors_forward then requires one too.  No effect for fp32;
- * applies to ranks up to 64 (above, the layer already runs as two passes).
- * The weight gradient always splits such a wave: its pieces' partial G tiles
- * go through the same rank-r products and atomics as whole tiles. */
+ * writes its fp32 partial sums (256 KiB) to the workspace; a small reduction
+ * launch adds a tile's pieces in a fixed order, adds the bias and rounds
+ * once to bf16, so results stay bitwise reproducible.  The partials are
+ * bounded so that the whole workspace (transposed mask, padded B copy and
+ * partials) stays below R*C/4 bytes, an eighth of the bf16 merged weight
+ * the layer exists not to store: when that budget cannot hold two pieces of
+ * every tile of the short wave, fewer pieces are used, or none (the call
+ * then runs as without the flag).  lors_workspace_bytes accounts for the
+ * partials, and lors_forward requires a workspace when there are any.  No
+ * effect for fp32; applies to ranks up to 64 (above, the layer already runs
+ * as two passes).  The weight gradient always splits such a wave, with no
+ * workspace: its pieces' partial G tiles go through the same rank-r products
+ * and atomics as whole tiles. */
 #define LORS_FLAG_SPLIT_LAST_WAVE 0x8u
 
 /*
  * Problem description.
  *   R (out features) >= 1, C (in features) >= 1, L (tokens) >= 0,
- *   1 <= r <= 128, every extent < 2^31, scale finite.
+ *   1 <= r <= 128, every extent < 2^31, scale finite, and every argument's
+ *   byte count (products L*C, L*R, R*C times 4) at most 2^60; otherwise
+ *   LORS_ERR_SHAPE.
  *   bf16: R % 8 == 0 and C % 8 == 0;  fp32: R % 4 == 0 and C % 4 == 0
  *   (16-byte rows); otherwise LORS_ERR_UNSUPPORTED.
  */
@@ -178,7 +185,11 @@ size_t lors_mask_packed_bytes(int64_t R, int64_t C);
  * LORS_MASK_2_4, `first_bad` (device, one int64) is required and receives the
  * linear index i*(C/4)+g of the first group that does not keep exactly two
  * entries, or -1 if every group is valid; for the bitmap it may be NULL (it is
- * then left untouched) or receives -1.  Asynchronous on `stream`.
+ * then left untouched) or receives -1.  Asynchronous on `stream`: the call
+ * returns LORS_OK once the work is queued and never LORS_ERR_NOT_2_4; the
+ * caller reads *first_bad after the stream work completes.  When it is >= 0
+ * the packed words are unspecified (an invalid group is not representable
+ * in the 2:4 layout) and must not be passed to the compute calls.
  * The mask M is the one of Section 2.1 and Algorithm 1 (kept = nonzero).
  */
 lors_status_t lors_mask_pack(const uint8_t* dense, int64_t R, int64_t C,
@@ -191,8 +202,9 @@ lors_status_t lors_mask_unpack(const uint32_t* packed, int64_t R, int64_t C,
 
 /*
  * Device mask derivation M = (W != 0) from the weight itself, as the paper's
- * algorithms and listing do (`weight != 0`); -0 counts as zero.  W has dtype
- * `dtype`.  `first_bad` as for lors_mask_pack.  Asynchronous.
+ * algorithms and listing do (`weight != 0`); -0 counts as zero and NaN as
+ * nonzero (IEEE comparison).  W has dtype `dtype`.  `first_bad` as for
+ * lors_mask_pack, with the same asynchronous contract.
  */
 lors_status_t lors_mask_from_weight(const void* W, int32_t dtype, int64_t R,
                                     int64_t C, int32_t mask_format,
@@ -218,6 +230,8 @@ lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C
  * LORS_FLAG_SPLIT_LAST_WAVE the fp32 partial sums of split tiles (forward and
  * dX; the forward uses only this last part, so a workspace shared by all
  * calls keeps the transposed mask), each part rounded up to 256; 0 for fp32.
+ * Without the straight-through flag the total stays below R*C/4 whenever the
+ * transposed mask and the padded B alone do (every shape with R*C >= 64 R r8).
  * (size_t)-1 if p is invalid.  The workspace must be
  * 16-byte aligned, must not overlap any argument, and is overwritten; its
  * contents on return are unspecified.  lors_forward needs one only with

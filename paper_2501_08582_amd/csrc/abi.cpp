@@ -17,6 +17,20 @@ namespace {
 
 constexpr int64_t kMaxExtent = (int64_t(1) << 31) - 1;
 constexpr int64_t kMaxRank = 128;
+// Largest byte count of any one argument.  Extents are below 2^31 each, so a
+// product of two of them and an element size can exceed int64_t; every byte
+// count is therefore checked against this bound before it is formed, and
+// sums of a few such counts stay far from overflow.
+constexpr int64_t kMaxBytes = int64_t(1) << 60;
+
+// a * b * es when it is at most kMaxBytes (a, b >= 0, es in 1..8), else -1.
+int64_t bytes_of(int64_t a, int64_t b, int64_t es) {
+    int64_t ab = 0, abe = 0;
+    if (a < 0 || b < 0 || __builtin_mul_overflow(a, b, &ab) || __builtin_mul_overflow(ab, es, &abe) ||
+        abe > kMaxBytes)
+        return -1;
+    return abe;
+}
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -48,6 +62,10 @@ lors_status_t check_problem(const lors_problem_t* p) {
     if (!valid_format(p->mask_format)) return LORS_ERR_MASK_FORMAT;
     if (p->R < 1 || p->C < 1 || p->L < 0 || p->r < 1 || p->r > kMaxRank) return LORS_ERR_SHAPE;
     if (p->R > kMaxExtent || p->C > kMaxExtent || p->L > kMaxExtent) return LORS_ERR_SHAPE;
+    // every argument's byte count (fp32 outputs are 4 bytes per element
+    // whatever the problem dtype) must be representable
+    if (bytes_of(p->L, p->C, 4) < 0 || bytes_of(p->L, p->R, 4) < 0 || bytes_of(p->R, p->C, 4) < 0)
+        return LORS_ERR_SHAPE;
     if (!std::isfinite(p->scale)) return LORS_ERR_SHAPE;
     if (p->mask_format == LORS_MASK_2_4 && (p->C % 4) != 0) return LORS_ERR_MASK_FORMAT;
     if ((p->flags & ~(LORS_FLAG_REUSE_MASK_T | LORS_FLAG_BWD_STE | LORS_FLAG_FWD_SPARSE_MFMA |
@@ -99,8 +117,8 @@ const char* lors_status_string(int status) {
 int lors_version(void) { return 10000; }
 
 size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
-    if (R < 0 || C < 0) return 0;
-    return static_cast<size_t>(R * words_per_row(C) * 4);
+    const int64_t n = (C < 0) ? -1 : bytes_of(R, words_per_row(C), 4);
+    return n < 0 ? 0 : static_cast<size_t>(n);
 }
 
 // bf16 backward workspace, each part rounded up to 256 bytes: the
@@ -122,16 +140,26 @@ static size_t bpad_bytes(const lors_problem_t* p) {
     if (p->r % 8 == 0) return 0;
     return static_cast<size_t>((2 * p->R * padded_rank(p->r) + 255) / 256 * 256);
 }
+// Bytes the fp32 partial sums of split tiles may use.  With the transposed
+// mask and the padded copy of B, the workspace then stays below R*C/4
+// bytes, an eighth of the merged weight the layer never stores (the
+// straight-through buffers, which grow with L, come on top).  When the
+// budget is short the split uses fewer pieces, or none.
+static int64_t split_budget(const lors_problem_t* p) {
+    const int64_t b = p->R * p->C / 4 - static_cast<int64_t>(mt_bytes(p) + bpad_bytes(p)) - 256;
+    return b > 0 ? b : 0;
+}
 // fp32 partial sums of the forward's or dX's split tiles (the larger of the
 // two; the calls run one after the other), with LORS_FLAG_SPLIT_LAST_WAVE.
 static size_t split_bytes(const lors_problem_t* p) {
     if ((p->flags & LORS_FLAG_SPLIT_LAST_WAVE) == 0u || p->dtype != LORS_DTYPE_BF16 || p->L == 0) return 0;
     const int64_t tl = (p->L + 255) / 256;
+    const int64_t budget = split_budget(p);
     int64_t fwd = 0, dx = 0;
     if (p->r <= 64 && (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) == 0u)
-        fwd = lors::split_part_bytes(lors::tail_split(tl * ((p->R + 255) / 256), (p->C + 63) / 64));
+        fwd = lors::split_part_bytes(lors::tail_split(tl * ((p->R + 255) / 256), (p->C + 63) / 64, budget));
     if (padded_rank(p->r) <= 64)
-        dx = lors::split_part_bytes(lors::tail_split(tl * ((p->C + 255) / 256), (p->R + 63) / 64));
+        dx = lors::split_part_bytes(lors::tail_split(tl * ((p->C + 255) / 256), (p->R + 63) / 64, budget));
     return static_cast<size_t>(fwd > dx ? fwd : dx);
 }
 size_t lors_workspace_bytes(const lors_problem_t* p) {
@@ -154,6 +182,7 @@ static void* split_region(const lors_problem_t* p, void* workspace) {
 static lors_status_t check_mask_args(int64_t R, int64_t C, int32_t fmt) {
     if (!valid_format(fmt)) return LORS_ERR_MASK_FORMAT;
     if (R < 0 || C < 0 || R > kMaxExtent || C > kMaxExtent) return LORS_ERR_SHAPE;
+    if (bytes_of(R, C, 4) < 0) return LORS_ERR_SHAPE;  // the dense mask and an fp32 weight
     if (fmt == LORS_MASK_2_4 && (C % 4) != 0) return LORS_ERR_MASK_FORMAT;
     return LORS_OK;
 }
@@ -205,7 +234,7 @@ lors_status_t lors_mask_from_weight(const void* W, int32_t dtype, int64_t R, int
 
 lors_status_t lors_mask_pack_host(const uint8_t* dense, int64_t R, int64_t C, int32_t mask_format,
                                   uint32_t* packed, int64_t* first_bad) {
-    if ((dense == nullptr && R * C > 0) || (packed == nullptr && R * C > 0)) return LORS_ERR_NULL;
+    if ((dense == nullptr || packed == nullptr) && R > 0 && C > 0) return LORS_ERR_NULL;
     lors_status_t st = check_mask_args(R, C, mask_format);
     if (st != LORS_OK) return st;
     const int64_t wpr = words_per_row(C);
@@ -240,7 +269,7 @@ lors_status_t lors_mask_pack_host(const uint8_t* dense, int64_t R, int64_t C, in
 
 lors_status_t lors_mask_unpack_host(const uint32_t* packed, int64_t R, int64_t C, int32_t mask_format,
                                     uint8_t* dense) {
-    if ((dense == nullptr && R * C > 0) || (packed == nullptr && R * C > 0)) return LORS_ERR_NULL;
+    if ((dense == nullptr || packed == nullptr) && R > 0 && C > 0) return LORS_ERR_NULL;
     lors_status_t st = check_mask_args(R, C, mask_format);
     if (st != LORS_OK) return st;
     const int64_t wpr = words_per_row(C);
@@ -305,6 +334,7 @@ lors_status_t lors_forward(const lors_problem_t* p, const void* X, const void* W
     a.sparse_mfma = (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) != 0u;
     a.X = X; a.W = W; a.M = M_packed; a.B = B; a.A = A; a.bias = bias; a.Y = Y;
     a.split_ws = need ? split_region(p, workspace) : nullptr;
+    a.split_budget = split_budget(p);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return from_hip(p->dtype == LORS_DTYPE_BF16 ? lors::launch_fwd_bf16(a, s) : lors::launch_fwd_f32(a, s));
 }
@@ -359,6 +389,7 @@ lors::LayerArgs layer_args(const lors_problem_t* p, const void* dY, const void* 
                   ? static_cast<uint8_t*>(workspace) + mt_bytes(p) + ste_bytes(p)
                   : nullptr;
     a.split_ws = split_region(p, workspace);
+    a.split_budget = split_budget(p);
     return a;
 }
 

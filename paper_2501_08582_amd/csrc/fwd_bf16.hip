@@ -402,7 +402,7 @@ hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     // a partial last wave of tiles is cut over K when the caller gave room
     // for the pieces' partial sums (one pass only: ranks up to 64)
     TailSplit sp{tiles_m * tiles_n, 1, tiles_m * tiles_n};
-    if (a.split_ws != nullptr && !PASS2 && a.r <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.C + BK - 1) / BK);
+    if (a.split_ws != nullptr && !PASS2 && a.r <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.C + BK - 1) / BK, a.split_budget);
     float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
     dim3 grid(sp.grid), block(NT);
     auto* X = (const uint16_t*)a.X;

@@ -407,7 +407,7 @@ template <int RK>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st) {
     const int tiles_m = (int)((a.R + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
-    const TailSplit sp = tail_split((int64_t)tiles_m * tiles_n, (a.L + BK - 1) / BK);
+    const TailSplit sp = tail_split((int64_t)tiles_m * tiles_n, (a.L + BK - 1) / BK, kNoPartials);
     dim3 grid(sp.grid), block(NT);
     auto* dY = (const uint16_t*)a.dY;
     auto* X = (const uint16_t*)a.X;

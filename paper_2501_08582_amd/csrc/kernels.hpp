@@ -32,21 +32,26 @@ struct LayerArgs {
     bool clear_grads;       // the bf16 dX launch also clears dB and dA (combined backward)
     int64_t r_grad;         // rank of dB and dA (the caller's r; the dX passes change a.r)
     void* split_ws;         // fp32 partial sums of split tiles (forward, dX), or nullptr: no split
+    int64_t split_budget;   // bytes of split_ws the partial sums may use
 };
 
 // Split of a grid of `tiles` output tiles whose K-loop has nk steps.  Whole
 // waves of tiles (one per CU) run unsplit; a last, partial wave that fills at
 // most half of the CUs is cut over K into `split` pieces per tile -- as many
-// as fill the CUs, at most 8, each at least 4 K-steps -- so that it does not
-// leave most of the chip idle.  n_full: the tiles that run whole; the grid
-// has n_full + (tiles - n_full) * split workgroups.
+// as fill the CUs, at most 8, each at least 4 K-steps, and no more than the
+// pieces whose 256 KiB of fp32 partial sums fit in `max_part_bytes` (a
+// kernel whose pieces need no partials passes kNoPartials) -- so that it
+// does not leave most of the chip idle.  n_full: the tiles that run whole;
+// the grid has n_full + (tiles - n_full) * split workgroups.
 struct TailSplit {
     int n_full, split, grid;
 };
-TailSplit tail_split(int64_t tiles, int64_t nk);
+constexpr int64_t kNoPartials = INT64_MAX;
+constexpr int64_t kPieceBytes = 256 * 256 * 4;  // fp32 partials of one piece
+TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes);
 // Bytes of fp32 partial sums a split grid of 256 x 256 tiles writes.
 inline int64_t split_part_bytes(const TailSplit& t) {
-    return t.split > 1 ? (int64_t)(t.grid - t.n_full) * 256 * 256 * 4 : 0;
+    return t.split > 1 ? (int64_t)(t.grid - t.n_full) * kPieceBytes : 0;
 }
 // out (rows x cols, bf16) on the split tiles = the sum of their pieces'
 // partials in piece order (+ bias[col] when bias is not null), rounded once.

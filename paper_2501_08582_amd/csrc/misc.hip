@@ -309,7 +309,7 @@ hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, in
     return hipGetLastError();
 }
 
-TailSplit tail_split(int64_t tiles, int64_t nk) {
+TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes) {
     // compute units of the current device, read once per device (calls from
     // several host threads may both read it; they store the same value)
     static std::atomic<int> cus_of[64];
@@ -326,6 +326,10 @@ TailSplit tail_split(int64_t tiles, int64_t nk) {
     int64_t s = cus / tail;
     if (s > 8) s = 8;
     if (s > nk / 4) s = nk / 4;
+    if (max_part_bytes != kNoPartials) {
+        const int64_t fit = max_part_bytes / (tail * kPieceBytes);
+        if (s > fit) s = fit;
+    }
     if (s < 2) return t;
     t.n_full = (int)(tiles - tail);
     t.split = (int)s;

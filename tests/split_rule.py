@@ -1,0 +1,47 @@
+"""The library's rule for splitting a short last wave of output tiles over K
+(as documented in include/lors.h), restated for the tests: which shapes split,
+into how many pieces, and which output tiles run in pieces."""
+
+
+def up256(n):
+    return -(-n // 256) * 256
+
+
+def split_budget(R, C, r):
+    """Bytes the split partials may use: the workspace (transposed mask,
+    padded copy of B, partials) stays below R*C/4."""
+    mt = up256(C * -(-R // 32) * 4)
+    bpad = up256(2 * R * (-(-r // 8) * 8)) if r % 8 else 0
+    return max(0, R * C // 4 - mt - bpad - 256)
+
+
+def pieces(tiles, nk, budget, cus=256):
+    """Pieces per tile of the short last wave (1: no split)."""
+    tail = tiles % cus
+    if tail == 0 or 2 * tail > cus:
+        return 1
+    s = min(8, cus // tail, nk // 4, budget // (tail * 256 * 256 * 4))
+    return s if s >= 2 else 1
+
+
+def split_bytes(tiles, nk, budget, cus=256):
+    s = pieces(tiles, nk, budget, cus)
+    return (tiles % cus) * s * 256 * 256 * 4 if s > 1 else 0
+
+
+def split_tiles(rows, cols, cus=256, group_m=4):
+    """(row0, col0) of the output tiles that run in pieces, given that the
+    grid splits: the logical tiles past the whole waves, mapped to tiles in
+    the kernels' grouped order (group_m tile rows at a time, column-major
+    inside a group)."""
+    tm_n, tn_n = -(-rows // 256), -(-cols // 256)
+    tiles = tm_n * tn_n
+    out = []
+    for t in range(tiles - tiles % cus, tiles):
+        per_group = group_m * tn_n
+        g = t // per_group
+        first = g * group_m
+        gsz = min(tm_n - first, group_m)
+        within = t - g * per_group
+        out.append((256 * (first + within % gsz), 256 * (within // gsz)))
+    return out

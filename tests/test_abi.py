@@ -294,38 +294,100 @@ def test_no_weak_symbol_defined_twice():
     pbuild._check_no_shared_weak_symbols(objs)
 
 
-def _tail_split_bytes(tiles, nk, cus=256):
-    """Partials of a split grid: a last, partial wave of at most half the CUs
-    is cut into min(8, cus // tail, nk // 4) pieces per tile (when >= 2)."""
-    tail = tiles % cus
-    if tail == 0 or 2 * tail > cus:
-        return 0
-    s = min(8, cus // tail, nk // 4)
-    return tail * s * 256 * 256 * 4 if s >= 2 else 0
+from split_rule import split_budget as _split_budget  # noqa: E402
+from split_rule import split_bytes as _tail_split_bytes  # noqa: E402
 
 
 def test_workspace_query_split_last_wave(lib):
     F = _lib.FLAG_SPLIT_LAST_WAVE
     for R, C, L, r in [(5120, 5120, 4096, 64), (4096, 1024, 4352, 16), (4104, 1000, 4300, 5), (4096, 4096, 4096, 16),
-                       (256, 256, 256, 8), (4096, 1024, 4352, 100), (13824, 5120, 4096, 64)]:
+                       (256, 256, 256, 8), (4096, 1024, 4352, 100), (13824, 5120, 4096, 64), (16384, 16384, 4352, 16),
+                       (65536, 8192, 4352, 64), (8192, 65536, 4352, 16), (32768, 16384, 4352, 16),
+                       # the GPU split tests' shapes
+                       (65792, 1024, 300, 16), (1024, 65792, 256, 64), (1024, 65792, 200, 5),
+                       (1024, 65792, 256, 100)]:
         base = _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r))
         tl = -(-L // 256)
-        fwd = _tail_split_bytes(tl * -(-R // 256), -(-C // 64)) if r <= 64 else 0
-        dx = _tail_split_bytes(tl * -(-C // 256), -(-R // 64)) if -(-r // 8) * 8 <= 64 else 0
+        budget = _split_budget(R, C, r)
+        fwd = _tail_split_bytes(tl * -(-R // 256), -(-C // 64), budget) if r <= 64 else 0
+        dx = _tail_split_bytes(tl * -(-C // 256), -(-R // 64), budget) if -(-r // 8) * 8 <= 64 else 0
         assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=F)) == base + max(fwd, dx), (R, C, L, r)
-    # 5120 x 5120 at 4096 tokens: 320 tiles, 64 in 4 pieces each, 64 MiB of partials
-    assert _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64, flags=F)) - \
-        _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64)) == 64 << 20
+    # 5120 x 5120 at 4096 tokens: 320 tiles, a short wave of 64; two pieces of
+    # each would need 32 MiB against a budget of about 3 MiB, so no split
+    assert _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64, flags=F)) == \
+        _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64))
+    # 8192 x 65536 at 4352 tokens: 17 x 32 = 544 forward tiles, a short wave
+    # of 32; the budget (64 MiB less 256 bytes) holds 7 pieces of each: 56 MiB
+    assert _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16, flags=F)) - \
+        _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16)) == 56 << 20
+    # 32768 x 16384: the dX grid (17 x 64 tiles, a short wave of 64) is cut
+    # into 3 pieces per tile (48 MiB), not the 4 that would fill the CUs
+    assert _lib.workspace_bytes(_p(R=32768, C=16384, L=4352, r=16, flags=F)) - \
+        _lib.workspace_bytes(_p(R=32768, C=16384, L=4352, r=16)) == 48 << 20
     # no effect for fp32, and none without tokens
     assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32, flags=F)) == 0
     assert _lib.workspace_bytes(_p(L=0, flags=F)) == _lib.workspace_bytes(_p(L=0))
 
 
+def _every_layer_shape():
+    """The benchmark workloads and the sweep's Llama-3-8B layer (q, o 4096 x
+    4096; k, v 1024 x 4096; gate, up 14336 x 4096; down 4096 x 14336 at
+    4 x 512 .. 4 x 2048 tokens, r 16 .. 64)."""
+    from paper_2501_08582_amd import synth
+    out = [(w.R, w.C, w.L, w.r, w.mask == "2:4") for w in synth.WORKLOADS.values() if w.dtype == "bf16"]
+    for R, C in ((4096, 4096), (1024, 4096), (14336, 4096), (4096, 14336)):
+        for seq in (512, 1024, 2048):
+            for r in (16, 32, 64):
+                out.append((R, C, 4 * seq, r, False))
+    return out
+
+
+@pytest.mark.parametrize("R,C,L,r,two_four", _every_layer_shape())
+def test_workspace_stays_far_below_the_merged_weight(lib, R, C, L, r, two_four):
+    """The library's scratch never approaches the R x C merged weight it
+    exists not to store: below R*C/4 bytes with or without the split flag,
+    below 2*R*C (the bf16 merged weight) with the straight-through buffers."""
+    fmt = _lib.MASK_2_4 if two_four else _lib.MASK_BITMAP
+    F = _lib.FLAG_SPLIT_LAST_WAVE
+    for flags in (0, F, F | _lib.FLAG_REUSE_MASK_T, F | (_lib.FLAG_FWD_SPARSE_MFMA if two_four else 0)):
+        n = _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, mask_format=fmt, flags=flags))
+        assert n < R * C // 4, (flags, n)
+    n = _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, mask_format=fmt, flags=F | _lib.FLAG_BWD_STE))
+    assert n < 2 * R * C
+
+
+@pytest.mark.parametrize("R,C,L", [((1 << 31) - 1, (1 << 31) - 1, 1), (8, (1 << 31) - 8, (1 << 31) - 1),
+                                   ((1 << 31) - 8, 8, (1 << 31) - 1), (1 << 30, 1 << 30, 8)])
+def test_extents_whose_byte_counts_overflow_are_rejected(lib, R, C, L):
+    """Each extent is below 2^31, but products such as L*C*4 exceed what a
+    64-bit byte count may hold (2^60 here): rejected as a shape error before
+    any pointer is used, and the workspace query reports an invalid problem."""
+    p = _p(R=R, C=C, L=L)
+    assert _fwd(p, _ptrs(6)) == _lib.ERR_SHAPE
+    assert _bwd(p, _ptrs(9)) == _lib.ERR_SHAPE
+    assert _lib.workspace_bytes(p) == 2**64 - 1
+    L_ = _lib.lib()
+    # the mask calls bound R*C the same way (only when R*C*4 > 2^60)
+    if R * C * 4 > 1 << 60:
+        assert L_.lors_mask_pack(BASE, R, C, 0, BASE + GAP, None, None) == _lib.ERR_SHAPE
+        # an fp32 weight of (2^31 - 1)^2 elements is 2^64 bytes
+        for dtype in (_lib.DTYPE_BF16, _lib.DTYPE_F32):
+            assert L_.lors_mask_from_weight(BASE, dtype, R, C, 0, BASE + GAP, None, None) == _lib.ERR_SHAPE
+        assert L_.lors_mask_unpack(BASE, R, C, 0, BASE + GAP, None) == _lib.ERR_SHAPE
+        assert _lib.mask_packed_bytes(R, C) == 4 * R * ((C + 31) // 32)
+
+
 def test_forward_requires_workspace_with_split_flag(lib):
     # validation happens before any HIP call, so this runs without a GPU
-    p = _p(R=4096, C=1024, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
+    # 8192 x 65536 at 4352 tokens splits its forward's short wave (see above)
+    p = _p(R=8192, C=65536, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
     need = _lib.workspace_bytes(p)
-    assert need > 0
+    assert need > _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16))
+    # a shape whose budget holds no pieces runs as without the flag, and the
+    # forward then needs no workspace: rejected only for its null pointers
+    q = _p(R=4096, C=1024, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
+    assert _lib.workspace_bytes(q) == _lib.workspace_bytes(_p(R=4096, C=1024, L=4352, r=16))
+    assert _lib.forward(q, None, 1 << 40, 1 << 41, 1 << 42, 1 << 43, None, 1 << 44, None, 0, None) == _lib.ERR_NULL
     fake = 1 << 40  # 16-byte aligned, never dereferenced
     args = [fake + i * (1 << 32) for i in range(6)]
     st = _lib.forward(p, args[0], args[1], args[2], args[3], args[4], None, args[5], None, 0, None)

@@ -13,7 +13,7 @@ torch = pytest.importorskip("torch")
 from oracle import lors as olors  # noqa: E402
 from oracle import masks as omasks  # noqa: E402
 from paper_2501_08582_amd import ops, synth  # noqa: E402
-from gpu_helpers import TOL, dev_to_f64, oracle_full, relerr, to_dev, to_f64  # noqa: E402
+from gpu_helpers import TOL, dev_to_f64, oracle_full, relerr, to_dev, to_f64, worst_tile  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -52,9 +52,21 @@ def _check_all(inp, bias=None, sparse_mfma=False):
     }
     if bias is not None:
         errs["dbias"] = relerr(dev_to_f64(dbias), rdbias)
-    print(inp.wl.name, (inp.wl.R, inp.wl.C, inp.wl.L, inp.wl.r), errs, flush=True)
+    # every 256 x 256 output tile of Y and dX, and every 256-row block of dB
+    # and 256-column block of dA, on its own: one wrong tile must not hide in
+    # the norm of the whole output
+    tiles = {
+        "Y tile": worst_tile(dev_to_f64(Y), rY),
+        "dX tile": worst_tile(dev_to_f64(dX), rdX),
+        "dB rows": worst_tile(dev_to_f64(dB), rdB, (256, rdB.shape[1] or 1)),
+        "dA cols": worst_tile(dev_to_f64(dA), rdA, (rdA.shape[0] or 1, 256)),
+    }
+    print(inp.wl.name, (inp.wl.R, inp.wl.C, inp.wl.L, inp.wl.r), errs,
+          {k: f"{e:.2e}@{tuple(int(i) for i in at)}" for k, (e, at) in tiles.items()}, flush=True)
     for k, e in errs.items():
         assert e <= tol, f"{k}: rel err {e:.3e} > {tol}"
+    for k, (e, at) in tiles.items():
+        assert e <= tol, f"{k} {tuple(int(i) for i in at)}: rel err {e:.3e} > {tol}"
     return errs
 
 
@@ -547,17 +559,40 @@ def test_weight_gradient_tail_split(R, C, L, r, mask):
 
 
 # ---------------------------------------------------------------------------
-# LORS_FLAG_SPLIT_LAST_WAVE: forward and dX tiles of a partial last wave cut
-# over K, fp32 partials reduced in a fixed order.  4352 tokens x 4096 outputs
-# is 17 x 16 = 272 forward tiles (256 whole, 16 in pieces); dX over 1024
-# inputs is 68 tiles, all in pieces; the weight gradient's 64 tiles too.
+# LORS_FLAG_SPLIT_LAST_WAVE: forward and dX tiles of a short last wave cut
+# over K, fp32 partials reduced in a fixed order, within a workspace budget
+# of R*C/4 bytes.  Shapes whose grids end in a short wave that the budget can
+# split (tests/split_rule.py restates the rule; test_abi checks the library
+# against it):
+#   65792 x 1024, 300 tokens: forward 2 x 257 tiles (2 in 4 pieces), dX 2 x 4
+#     tiles (all 8 in 4 pieces);
+#   1024 x 65792, 256 tokens: forward 4 tiles in 8 pieces, dX 257 tiles (1 in
+#     4 pieces); rank 5 adds the padded copy of B; rank 100 runs two passes
+#     and is not split.
+# Split tiles must agree with the unsplit call within one bf16 ulp (the two
+# differ only in fp32 summation order), every other tile bit for bit, and
+# both with the oracle; W is unpruned so that the split pieces also see data
+# at masked positions.
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("R,C,L,r,mask,bias", [(4096, 1024, 4352, 16, "magnitude", False),
-                                               (4104, 1000, 4300, 5, "magnitude", True),
-                                               (4096, 1024, 4352, 64, "2:4", False),
-                                               (4096, 1024, 4352, 100, "magnitude", False)])
+def _ulp_close(a, b):
+    """|a - b| <= one bf16 ulp of max(|a|, |b|), plus 2^-12 of the output's
+    RMS for results near cancellation."""
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    m = np.maximum(np.abs(a), np.abs(b))
+    ulp = np.exp2(np.floor(np.log2(np.maximum(m, 1e-38))) - 7)
+    rms = np.sqrt(np.mean(b * b)) if b.size else 0.0
+    return np.abs(a - b) <= ulp + rms / 4096
+
+
+@pytest.mark.parametrize("R,C,L,r,mask,bias", [(65792, 1024, 300, 16, "magnitude", True),
+                                               (1024, 65792, 256, 64, "2:4", False),
+                                               (1024, 65792, 200, 5, "magnitude", False),
+                                               (1024, 65792, 256, 100, "magnitude", False)])
 def test_split_last_wave(R, C, L, r, mask, bias):
+    import split_rule
+    from gpu_helpers import unprune as _unprune
     inp = _inputs("llama2_7b_q_proj", R=R, C=C, r=r, mask=mask, seed=1500 + r, L=L)
+    inp.W = _unprune(inp.W, inp.M, "bf16", seed=r)
     dt = "bf16"
     X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
     fmt = FMT[mask]
@@ -576,11 +611,105 @@ def test_split_last_wave(R, C, L, r, mask, bias):
     dX1, _, _, _ = ops.backward(dY, X, W, M, B, A, s, fmt, split_last_wave=True)
     torch.cuda.synchronize()
     assert torch.equal(Y, Y1) and torch.equal(dX, dX1)
-    rY, rdX, rdB, rdA, _ = oracle_full(inp, s, to_f64(bias_bits, dt) if bias else None)
-    errs = {"Y": relerr(dev_to_f64(Y), rY), "dX": relerr(dev_to_f64(dX), rdX),
-            "dB": relerr(dev_to_f64(dB), rdB), "dA": relerr(dev_to_f64(dA), rdA),
-            "Y vs unsplit": relerr(dev_to_f64(Y), dev_to_f64(Y0)),
-            "dX vs unsplit": relerr(dev_to_f64(dX), dev_to_f64(dX0))}
-    print(errs, flush=True)
-    for k, e in errs.items():
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    budget = split_rule.split_budget(R, C, r)
+    tl = -(-L // 256)
+    f = lambda a: to_f64(a, dt)  # noqa: E731
+    bias64 = f(bias_bits) if bias else None
+    checked = 0
+    for name, got, ref0, N, K, ok in (("Y", Y, Y0, R, C, r <= 64), ("dX", dX, dX0, C, R, -(-r // 8) * 8 <= 64)):
+        g, u = dev_to_f64(got), dev_to_f64(ref0)
+        split = ok and split_rule.pieces(tl * -(-N // 256), -(-K // 64), budget, cus) > 1
+        rects = split_rule.split_tiles(L, N, cus) if split else []
+        inside = np.zeros(g.shape, dtype=bool)
+        for m0, n0 in rects:
+            inside[m0:m0 + 256, n0:n0 + 256] = True
+        assert np.array_equal(g[~inside], u[~inside]), f"{name}: a tile outside the short wave changed"
+        assert np.all(_ulp_close(g[inside], u[inside])), f"{name}: split tiles differ by more than one bf16 ulp"
+        for m0, n0 in rects:
+            tok = np.arange(m0, min(m0 + 256, L))
+            idx = np.arange(n0, min(n0 + 256, N))
+            if name == "Y":
+                want = olors.forward_entries(f(inp.X), f(inp.W), inp.M, f(inp.B), f(inp.A), s, tok, idx, bias64)
+            else:
+                want = olors.dx_entries(f(inp.dY), f(inp.W), inp.M, f(inp.B), f(inp.A), s, tok, idx)
+            e = relerr(g[np.ix_(tok, idx)], want)
+            assert e <= TOL[dt], f"{name} split tile ({m0}, {n0}): rel err {e:.3e}"
+            checked += 1
+    rng = np.random.default_rng(R + L)
+    rows = np.sort(rng.choice(R, 4, replace=False))
+    cols = np.sort(rng.choice(C, 4, replace=False))
+    e_db = relerr(dev_to_f64(dB)[rows], olors.db_rows(f(inp.dY), f(inp.X), inp.M, f(inp.A), s, rows))
+    e_da = relerr(dev_to_f64(dA)[:, cols], olors.da_cols(f(inp.dY), f(inp.X), inp.M, f(inp.B), s, cols))
+    print({"split tiles checked": checked, "dB rows": e_db, "dA cols": e_da}, flush=True)
+    assert e_db <= TOL[dt] and e_da <= TOL[dt]
+    if r <= 64:
+        assert checked > 0, "the shape was meant to split"
+
+
+# ---------------------------------------------------------------------------
+# out-of-bounds writes: every output and the workspace sit inside a larger
+# buffer with 4 KiB guards on both sides.  Guards are filled with 0xA5 and the
+# outputs with 0xFF bytes (NaN in bf16 and fp32), so an unwritten output
+# element or a write past either end shows.
+# ---------------------------------------------------------------------------
+GUARD = 4096
+
+
+def _guarded(nelem, dtype, fill_out=0xFF):
+    esz = torch.tensor([], dtype=dtype).element_size()
+    n = nelem * esz
+    buf = torch.full((2 * GUARD + max(n, 16),), 0xA5, dtype=torch.uint8, device="cuda")
+    buf[GUARD:GUARD + n] = fill_out
+    return buf, buf[GUARD:GUARD + n].view(dtype)
+
+
+def _guards_intact(buf, n):
+    head = buf[:GUARD]
+    tail = buf[GUARD + n:]
+    return bool(torch.all(head == 0xA5).item()) and bool(torch.all(tail == 0xA5).item())
+
+
+@pytest.mark.parametrize("R,C,L,r,mask,bias,split", [
+    (520, 776, 300, 16, "magnitude", True, False),   # ragged in every dimension
+    (264, 520, 130, 112, "2:4", True, False),        # two rank passes (the second adds onto Y and dX)
+    (264, 1032, 77, 5, "magnitude", False, True),    # padded B in the workspace; no split (small R*C)
+    (1024, 65792, 200, 5, "magnitude", True, True),  # split forward and dX with partials in the workspace
+])
+def test_outputs_and_workspace_stay_in_bounds(R, C, L, r, mask, bias, split):
+    from paper_2501_08582_amd import _lib
+    inp = _inputs("llama2_7b_q_proj", R=R, C=C, r=r, mask=mask, seed=2000 + r, L=L)
+    dt = "bf16"
+    X, W, B, A, dY = (to_dev(t, dt) for t in (inp.X, inp.W, inp.B, inp.A, inp.dY))
+    fmt = FMT[mask]
+    M = ops.mask_pack(torch.from_numpy(inp.M).cuda(), fmt)
+    bias_bits = synth.f32_to_bf16_bits(np.random.default_rng(3).standard_normal(R).astype(np.float32)) if bias else None
+    bias_t = to_dev(bias_bits, dt) if bias else None
+    lfmt = _lib.MASK_2_4 if fmt == ops.TWO_FOUR else _lib.MASK_BITMAP
+    flags = _lib.FLAG_SPLIT_LAST_WAVE if split else 0
+    p = _lib.problem(R, C, L, r, inp.wl.scale, _lib.DTYPE_BF16, lfmt, flags)
+    nws = _lib.workspace_bytes(p)
+    bufs = {
+        "Y": _guarded(L * R, torch.bfloat16), "dX": _guarded(L * C, torch.bfloat16),
+        "dB": _guarded(R * r, torch.float32), "dA": _guarded(r * C, torch.float32),
+        "dbias": _guarded(R, torch.float32), "ws": _guarded(nws, torch.uint8, fill_out=0x5A),
+    }
+    ptr = {k: v[1].data_ptr() for k, v in bufs.items()}
+    st = torch.cuda.current_stream().cuda_stream
+    print("guarded", (R, C, L, r, mask, bias, split), "workspace", nws, flush=True)
+    _lib.check(_lib.forward(p, X.data_ptr(), W.data_ptr(), M.data_ptr(), B.data_ptr(), A.data_ptr(),
+                            bias_t.data_ptr() if bias else None, ptr["Y"], ptr["ws"], nws, st), "lors_forward")
+    _lib.check(_lib.backward(p, dY.data_ptr(), X.data_ptr(), W.data_ptr(), M.data_ptr(), B.data_ptr(),
+                             A.data_ptr(), ptr["dX"], ptr["dB"], ptr["dA"], ptr["dbias"], ptr["ws"], nws, st),
+               "lors_backward")
+    torch.cuda.synchronize()
+    for k, (buf, view) in bufs.items():
+        assert _guards_intact(buf, view.numel() * view.element_size()), f"{k}: a guard byte changed"
+    b64 = to_f64(bias_bits, dt) if bias else None
+    rY, rdX, rdB, rdA, rdbias = oracle_full(inp, inp.wl.scale, b64)
+    for k, ref in (("Y", rY), ("dX", rdX), ("dB", rdB), ("dA", rdA), ("dbias", rdbias)):
+        got = dev_to_f64(bufs[k][1]).reshape(ref.shape)
+        assert np.all(np.isfinite(got)), f"{k}: an element was not written"
+        e = relerr(got, ref)
         assert e <= TOL[dt], f"{k}: rel err {e:.3e}"

@@ -436,3 +436,37 @@ def test_gradient_init_uses_the_masked_gradient():
     assert np.allclose(GtG @ A0.T, proj @ GtG @ A0.T, atol=1e-10)
     ev = np.sort(np.linalg.eigvalsh(GtG))[::-1]
     assert np.isclose(np.trace(A0 @ GtG @ A0.T), ev[:r].sum(), rtol=1e-10)
+
+
+# ---------------------------------------------------------------------------
+# the sign convention of the initialisation's singular vectors (Section 2.4
+# fixes none; this repository's convention is: the entry of largest magnitude
+# in each row is positive, the first such entry on ties).  Literal rows.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("V,want", [
+    # largest entry already positive: unchanged
+    ([[0.1, -0.5, 0.9]], [[0.1, -0.5, 0.9]]),
+    # largest-magnitude entry negative: the whole row flips
+    ([[0.3, -0.8, 0.2]], [[-0.3, 0.8, -0.2]]),
+    # a tie in magnitude: the first index decides (here it is negative)
+    ([[-0.5, 0.5, 0.1]], [[0.5, -0.5, -0.1]]),
+    # a tie where the first index is positive: unchanged
+    ([[0.5, -0.5, 0.1]], [[0.5, -0.5, 0.1]]),
+    # an all-zero row stays zero (its sign is taken as +1)
+    ([[0.0, 0.0, 0.0]], [[0.0, 0.0, 0.0]]),
+    # several rows are treated independently
+    ([[1.0, -2.0], [-3.0, 1.0], [0.0, 4.0]], [[-1.0, 2.0], [3.0, -1.0], [0.0, 4.0]]),
+])
+def test_canonical_rows_literal(V, want):
+    got = lors.canonical_rows(np.array(V))
+    assert got.tolist() == want
+    # the input is not modified
+    assert np.array(V).tolist() == V
+
+
+def test_canonical_rows_empty_and_shape():
+    assert lors.canonical_rows(np.zeros((0, 5))).shape == (0, 5)
+    assert lors.canonical_rows(np.zeros((3, 0))).shape == (3, 0)
+    # a flipped row keeps its exact magnitudes (a sign change only)
+    v = np.array([[-0.25, 0.125, -1.5]])
+    assert lors.canonical_rows(v).tolist() == [[0.25, -0.125, 1.5]]
