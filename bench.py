@@ -71,6 +71,9 @@ def parse():
     ap.add_argument("--pmc-probe", action="store_true",
                     help="short program for hardware-counter runs: one step, a device copy of "
                          "COPY_BYTES (the calibration of the byte counters), one more step")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU work: print the HBM-traffic summary of --workload from the counter CSVs of two "
+                         "rocprofv3 --pmc runs of --pmc-probe (FETCH_SIZE, then WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -107,6 +110,45 @@ def measured_traffic(workload: str, kernel: str):
         if len(f) == 5 and f[0] == kernel:
             return int(f[3]) if f[4] == kernel_digest(kernel) else None
     return None
+
+
+def traffic_summary(workload: str, fetch_csv: str, write_csv: str, commands=()) -> str:
+    """The profiles/traffic_<workload>.txt text from the counter CSVs of two
+    --pmc-probe runs.  Each counter is calibrated on the probe's device copy of
+    COPY_BYTES (read and written once each); a kernel's figure is the mean of
+    its last two dispatches, the probe's two steps (a dX launch at set-up,
+    which writes the transposed mask, comes before them)."""
+    import csv
+
+    def per_kernel(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if len(copy) != 1:
+            raise ValueError(f"{path}: expected one calibration copy, found {len(copy)}")
+        vals = {}
+        for k in KERNEL_SOURCES:
+            v = [float(r["Counter_Value"]) for r in rows if f"::{k}<" in r["Kernel_Name"]]
+            if len(v) >= 2:
+                vals[k] = sum(v[-2:]) / 2
+        return copy[0], vals
+
+    cf, fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    cw, write = per_kernel(write_csv, "WRITE_SIZE")
+    ff, fw = COPY_BYTES / (cf * 1024), COPY_BYTES / (cw * 1024)
+    lines = [f"# HBM traffic per launch, {workload} (one layer step, bf16)",
+             "# Commands (repository root, TMPDIR=/tmp), one counter per run:"]
+    lines += [f"#   {c}" for c in commands]
+    lines += [f"# Calibration: the {COPY_BYTES}-byte device copy (__amd_rocclr_copyBuffer) reads",
+              f"#   FETCH_SIZE {cf:.1f} KiB and WRITE_SIZE {cw:.1f} KiB,",
+              f"#   so traffic = FETCH_SIZE * 1024 * {ff:.5f} + WRITE_SIZE * 1024 * {fw:.5f} bytes.",
+              "# Values are the mean of each kernel's last two dispatches (the probe run's two steps).",
+              "# kernel  fetch_KiB  write_KiB  traffic_bytes  source_digest"]
+    for k in KERNEL_SOURCES:
+        if k in fetch and k in write:
+            t = int(round(fetch[k] * 1024 * ff + write[k] * 1024 * fw))
+            lines.append(f"{k} {fetch[k]:.1f} {write[k]:.1f} {t} {kernel_digest(k)}")
+    return "\n".join(lines) + "\n"
 
 
 def cpu_baseline(inp, args):
@@ -156,6 +198,13 @@ def cpu_baseline(inp, args):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        cmds = [f"rocprofv3 --pmc {c} --output-format csv -d {os.path.dirname(f)} -o pmc "
+                f"-- python -u bench.py --pmc-probe --workload {args.workload}"
+                for c, f in zip(("FETCH_SIZE", "WRITE_SIZE"), args.traffic_from)]
+        cmds.append(f"python bench.py --workload {args.workload} --traffic-from {' '.join(args.traffic_from)}")
+        sys.stdout.write(traffic_summary(args.workload, *args.traffic_from, commands=cmds))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the layer shards by tokens, see the design notes)", file=sys.stderr)
@@ -248,35 +297,33 @@ def main():
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
 
-    # Per-kernel durations: each call issued K times back to back on the same
-    # stream between two events (the data half with the transposed mask
-    # already built, i.e. the dX kernel alone; the weight half is the dA/dB
-    # clear plus the G kernel).
-    def per_call(fn):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps
+    # Per-kernel durations inside the step: K more steps, each issued as its
+    # three calls -- the forward, the data half (the dX kernel alone, the
+    # transposed mask being built already) and the weight half (the dA/dB
+    # clear plus the G kernel) -- with an event on the launch stream before,
+    # between and after them.  Timing the calls in the step's own order
+    # keeps each kernel's cache state that of the training loop: a kernel
+    # repeated back to back finds much of its operands in the GPU's last-level
+    # cache and runs faster than it does after the others.  The markers cost a
+    # few microseconds, so the headline value above comes from the unmarked
+    # steps; these marked steps also give the per-step spread.
+    def marked_step(ev):
+        ev[0].record(stream)
+        layer.forward()
+        ev[1].record(stream)
+        layer.backward_data(reuse_mask_t=True)
+        ev[2].record(stream)
+        layer.backward_weight()
+        ev[3].record(stream)
 
-    # Per-step spread: the same step with its own pair of events around each
-    # iteration (markers between steps cost a few microseconds, so the
-    # headline value above comes from the unmarked run).
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    for a, b in evs:
-        a.record(stream)
-        step()
-        b.record(stream)
+    for ev in evs:
+        marked_step(ev)
     torch.cuda.synchronize()
-    per_step_us = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
-
-    avg = {"fwd": per_call(layer.forward),
-           "bwd_data": per_call(lambda: layer.backward_data(reuse_mask_t=True)),
-           "bwd_weight": per_call(layer.backward_weight)}
+    per_step_us = sorted(ev[0].elapsed_time(ev[3]) * 1e3 for ev in evs)
+    avg = {k: sum(ev[i].elapsed_time(ev[i + 1]) for ev in evs) / len(evs)
+           for i, k in enumerate(("fwd", "bwd_data", "bwd_weight"))}
     kflops = {"fwd": costs.fwd_flops(R, C, L, r), "bwd_data": costs.dx_flops(R, C, L, r),
               "bwd_weight": costs.ste_weight_flops(R, C, L, r) if args.ste else costs.g_flops(R, C, L, r)}
     kbytes = costs.min_hbm_bytes(R, C, L, r, elt=2 if dt == "bf16" else 4)
@@ -319,7 +366,8 @@ def main():
         "pct_mfma_peak": round(100.0 * value / peak, 2),
         "executed_tflops": round(executed / (ms_step * 1e-3) / 1e12, 2),
         "step_us_marked": {"median": round(per_step_us[len(per_step_us) // 2], 1),
-                           "min": round(per_step_us[0], 1)},
+                           "min": round(per_step_us[0], 1),
+                           "calls": "forward | data half (dX) | weight half (dA/dB clear + G)"},
         "peak_bytes": {
             "weight_buffers": costs.weight_buffer_bytes(R, C, r, elt),
             "saved_activation": costs.saved_activation_bytes(C, L, elt),
