@@ -288,6 +288,35 @@ lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY,
                                    float* dA, float* dbias, void* workspace,
                                    size_t workspace_bytes, void* stream);
 
+/*
+ * lors_backward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same computation, arguments (less
+ * the workspace), layouts, results and errors as lors_backward, with its
+ * scratch in a file-scope device array of LORS_NOALLOC_SCRATCH_BYTES that
+ * each GPU the library runs on holds from the library's first use on it until
+ * the process ends.  The call allocates nothing (no hipMalloc, no allocating
+ * library routine); the caller still passes every input and output.
+ *   - Problems whose lors_workspace_bytes exceeds LORS_NOALLOC_SCRATCH_BYTES
+ *     return LORS_ERR_WORKSPACE (validation happens on the host first, as
+ *     for every entry point).
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents: LORS_FLAG_REUSE_MASK_T is refused
+ *     (LORS_ERR_UNSUPPORTED), the transposed mask is rebuilt on every call,
+ *     and nothing in the array needs to start at zero.  Calls that overlap
+ *     in time on one GPU (different streams or host threads) race on the
+ *     array: serialise them.
+ *   - The array is the one of the device `stream` belongs to (the current
+ *     device for the null stream); its device address is looked up once per
+ *     device, on the first call there (LORS_ERR_HIP if that fails).
+ */
+#define LORS_NOALLOC_SCRATCH_BYTES (32u << 20)
+lors_status_t lors_backward_noalloc(const lors_problem_t* p, const void* dY,
+                                    const void* X, const void* W,
+                                    const uint32_t* M_packed, const void* B,
+                                    const void* A, void* dX, float* dB,
+                                    float* dA, float* dbias, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

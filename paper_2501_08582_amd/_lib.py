@@ -39,8 +39,9 @@ EXPORTED = (
     "lors_status_string", "lors_version", "lors_mask_packed_bytes", "lors_mask_pack",
     "lors_mask_unpack", "lors_mask_from_weight", "lors_mask_pack_host", "lors_mask_unpack_host",
     "lors_workspace_bytes", "lors_forward", "lors_backward", "lors_backward_data",
-    "lors_backward_weight",
+    "lors_backward_weight", "lors_backward_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class Problem(ctypes.Structure):
@@ -89,6 +90,7 @@ def _declare(lib) -> None:
         "lors_backward_data": (ctypes.c_int, [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
         "lors_backward_weight": (ctypes.c_int,
                                  [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+        "lors_backward_noalloc": (ctypes.c_int, [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -171,3 +173,7 @@ def backward_data(p: Problem, dY, W, M, B, A, dX, ws, ws_bytes, stream) -> int:
 def backward_weight(p: Problem, dY, X, M, B, A, dB, dA, dbias, ws, ws_bytes, stream) -> int:
     return lib().lors_backward_weight(ctypes.byref(p), dY, X, M, B, A, dB, dA, dbias, ws, ws_bytes,
                                       stream)
+
+
+def backward_noalloc(p: Problem, dY, X, W, M, B, A, dX, dB, dA, dbias, stream) -> int:
+    return lib().lors_backward_noalloc(ctypes.byref(p), dY, X, W, M, B, A, dX, dB, dA, dbias, stream)

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "lors.h"
 #include "kernels.hpp"
@@ -114,7 +115,7 @@ const char* lors_status_string(int status) {
     }
 }
 
-int lors_version(void) { return 10000; }
+int lors_version(void) { return 10100; }
 
 size_t lors_mask_packed_bytes(int64_t R, int64_t C) {
     const int64_t n = (C < 0) ? -1 : bytes_of(R, words_per_row(C), 4);
@@ -475,3 +476,79 @@ lors_status_t lors_backward_weight(const lors_problem_t* p, const void* dY, cons
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The backward without a caller-provided workspace, for callers that cannot
+// allocate device memory.  Its scratch is one file-scope device array per
+// GPU, shared by every call on that GPU.
+// ---------------------------------------------------------------------------
+namespace {
+
+static __device__ __align__(256) uint8_t scratch[LORS_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_of[kMaxDevices];  // device address of `scratch` per device, once looked up
+
+// The device whose queue `stream` feeds (the current device for the null
+// stream), and that device's address of `scratch`.  In host code the
+// array's name stands for a host-side shadow, not device memory, so the
+// device address is looked up -- once per device, with that device current --
+// and only that address is handed to kernels.
+hipError_t scratch_of_stream(hipStream_t stream, void** out) {
+    int dev = 0;
+    hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_of[dev] == nullptr) {
+        int cur = -1;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_of[dev] = p;
+    }
+    *out = g_scratch_of[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" lors_status_t lors_backward_noalloc(const lors_problem_t* p, const void* dY, const void* X,
+                                               const void* W, const uint32_t* M_packed, const void* B,
+                                               const void* A, void* dX, float* dB, float* dA, float* dbias,
+                                               void* stream) {
+    if (p == nullptr) return LORS_ERR_NULL;
+    const bool tok = p->L != 0;
+    if ((tok && (dY == nullptr || X == nullptr)) || W == nullptr || M_packed == nullptr || B == nullptr ||
+        A == nullptr || dB == nullptr || dA == nullptr)
+        return LORS_ERR_NULL;
+    lors_status_t st = check_backward(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, nullptr, 0);
+    // the only failure that a workspace would have avoided: the scratch size
+    if (st == LORS_ERR_WORKSPACE) st = LORS_OK;
+    if (st != LORS_OK) return st;
+    // the scratch keeps the previous call's contents, whoever made it
+    if ((p->flags & LORS_FLAG_REUSE_MASK_T) != 0u) return LORS_ERR_UNSUPPORTED;
+    const size_t need = lors_workspace_bytes(p);
+    if (need > LORS_NOALLOC_SCRATCH_BYTES) return LORS_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* ws = nullptr;
+    if (need > 0) {
+        const hipError_t e = scratch_of_stream(s, &ws);
+        if (e != hipSuccess) return LORS_ERR_HIP;
+    }
+    lors::LayerArgs a = layer_args(p, dY, X, W, M_packed, B, A, dX, dB, dA, dbias, ws);
+    const bool bf16 = p->dtype == LORS_DTYPE_BF16;
+    a.clear_grads = bf16 && !a.ste && dX != nullptr && tok;
+    hipError_t e = build_mt(a, bf16, s);
+    if (e == hipSuccess && dX) e = bf16 ? lors::launch_dx_bf16(a, s) : lors::launch_dx_f32(a, s);
+    if (e == hipSuccess) e = run_weight(a, bf16, s);
+    return from_hip(e);
+}

@@ -45,7 +45,7 @@ def test_status_strings(lib):
         s = _lib.string(code)
         assert s.startswith("LORS_")
     assert "unknown" in _lib.string(99)
-    assert lib.lors_version() == 10000
+    assert lib.lors_version() == 10100
 
 
 @pytest.mark.parametrize("R,C", [(1, 1), (3, 31), (3, 32), (5, 33), (4096, 14336)])
@@ -395,3 +395,50 @@ def test_forward_requires_workspace_with_split_flag(lib):
     st = _lib.forward(p, args[0], args[1], args[2], args[3], args[4], None, args[5], fake + 7 * (1 << 32), need - 1,
                       None)
     assert st == _lib.ERR_WORKSPACE
+
+
+# ---------------------------------------------------------------------------
+# lors_backward_noalloc: validated like lors_backward, before any HIP call
+# ---------------------------------------------------------------------------
+def _noalloc(p, ptrs, dbias=None):
+    dY, X, W, M, B, A, dX, dB, dA = ptrs
+    return _lib.backward_noalloc(p, dY, X, W, M, B, A, dX, dB, dA, dbias, None)
+
+
+def test_noalloc_validation(lib):
+    bp = _ptrs(9)
+    for k in [0, 1, 2, 3, 4, 5, 7, 8]:
+        bad = list(bp)
+        bad[k] = None
+        assert _noalloc(_p(), bad) == _lib.ERR_NULL
+    assert _noalloc(_p(dtype=3), bp) == _lib.ERR_DTYPE
+    assert _noalloc(_p(R=0), bp) == _lib.ERR_SHAPE
+    assert _noalloc(_p(R=60), bp) == _lib.ERR_UNSUPPORTED
+    bad = list(bp)
+    bad[6] += 8
+    assert _noalloc(_p(), bad) == _lib.ERR_ALIGN
+    bad = list(bp)
+    bad[8] = bad[7] + 16
+    assert _noalloc(_p(), bad) == _lib.ERR_ALIAS
+    # the shared scratch keeps other calls' contents: no reuse of the mask
+    assert _noalloc(_p(flags=_lib.FLAG_REUSE_MASK_T), bp) == _lib.ERR_UNSUPPORTED
+
+
+def test_noalloc_rejects_problems_beyond_its_scratch(lib):
+    # 16384 x 16392: the transposed mask alone is just over 32 MiB
+    big = _p(R=16384, C=16392, L=256, r=16)
+    assert _lib.workspace_bytes(big) > _lib.NOALLOC_SCRATCH_BYTES
+    assert _noalloc(big, _ptrs(9)) == _lib.ERR_WORKSPACE
+    # a problem that needs exactly the scratch's size fits (checked through
+    # the query only: a call would launch work on the fake pointers)
+    assert _lib.workspace_bytes(_p(R=16384, C=16384, L=256, r=16)) == _lib.NOALLOC_SCRATCH_BYTES
+    # the benchmark shapes fit
+    from paper_2501_08582_amd import synth
+    for w in synth.WORKLOADS.values():
+        fmt = _lib.MASK_2_4 if w.mask == "2:4" else _lib.MASK_BITMAP
+        dt = _lib.DTYPE_BF16 if w.dtype == "bf16" else _lib.DTYPE_F32
+        for flags in (0, _lib.FLAG_SPLIT_LAST_WAVE, _lib.FLAG_BWD_STE):
+            if flags == _lib.FLAG_BWD_STE and dt != _lib.DTYPE_BF16:
+                continue
+            p = _p(R=w.R, C=w.C, L=w.L, r=w.r, dtype=dt, mask_format=fmt, flags=flags)
+            assert _lib.workspace_bytes(p) <= _lib.NOALLOC_SCRATCH_BYTES, (w.name, flags)
