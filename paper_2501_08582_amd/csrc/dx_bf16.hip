@@ -19,7 +19,8 @@
 // MFMA slot carrying a fixed share of the next sub-step's operand reads and
 // merge arithmetic, one barrier per K-step before the last sub-step, which
 // interleaves the copies of stage kt+2 and the first sub-step of stage kt+1.
-// Requires r % 8 == 0 and r <= 64 (other ranks use the LDS-merge kernel).
+// Works on ranks that are multiples of 8, up to 64 per pass (the launcher pads
+// other ranks with a zero-filled copy of B and splits larger ones in two).
 #include "gemm_common.hpp"
 #include "kernels.hpp"
 
@@ -39,17 +40,29 @@ constexpr int DB = BM * kRow64;      // dY slab: 32 KiB
 constexpr int WB = BK * kRowBytes;   // W slab [k][n]: 32 KiB
 constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 
+// B slab [k][rank]: 64 rows of PITCH = 32*RKP bytes (ranks padded to 16*RKP;
+// RKP = RK, except 4 for RK = 3 so that a row holds a power of two of 16-byte
+// chunks).  Chunk q of row k is stored at chunk q ^ bswz(k): the merge reads
+// one chunk of 16 consecutive rows per 16 lanes, and with rows 32*RKP bytes
+// apart those rows would fall on only 8 / RKP of the 16 bank groups; the XOR
+// spreads them over all 16 (a 256-byte bank window holds 8 / RKP rows, and
+// bswz takes 2*RKP distinct values over 16 consecutive rows).
 template <int RK>
 struct Layout {
-    static constexpr int BB = BK * 32 * RK;        // B slab [k][r], pitch 2r <= 32*RK bytes
+    static constexpr int RKP = RK == 3 ? 4 : RK;
+    static constexpr int PITCH = 32 * RKP;
+    static constexpr int BB = BK * PITCH;          // B slab: 2 KiB per 16 ranks
     static constexpr int D = 0, W = DB, B = DB + WB, M = DB + WB + BB;
     static constexpr int STAGE = DB + WB + BB + MB;
     static constexpr int LUT = 2 * STAGE;
     static constexpr int SINK = LUT + 4096;        // 1 KiB target of padding copies
     static constexpr int TOTAL = SINK + 1024;
-    static constexpr int NB = (2 * RK + 3) / 4;    // B-slab copies per wave (r/8 copies in all)
+    static constexpr int NBC = BB / 1024;          // 1 KiB copies per B slab
+    static constexpr int NB = (NBC + 3) / 4;       // B-slab copies per wave
     static constexpr int COPIES = 16 + NB + 2;     // copies per wave per stage
     static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
+    // physical chunk of logical chunk q in B-slab row k
+    static __device__ __forceinline__ int bswz(int k, int q) { return q ^ ((k / (8 / RKP)) & (2 * RKP - 1)); }
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -102,16 +115,20 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const int wprT = (R + 31) >> 5;  // words per row of M^T
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * lane;
-    const int slab_b = 2 * r;        // bytes per B row in the slab
-    const int nbcopies = r >> 3;     // 1 KiB copies per B slab (64 rows x 2r bytes)
-    // B-slab copy q of this wave: its 16 bytes are row brow[q], byte bcol[q]
-    // of the [64][r] slab; rows of B are ldb elements apart in memory
+    // B-slab copy q of this wave lands at slab byte 1024*(4q + wave) + 16*lane,
+    // i.e. row brow[q], physical chunk p; it carries logical chunk
+    // bswz(brow, p) -- ranks 8*that .. +7 of B row k0 + brow[q] (rows of B are
+    // ldb elements apart in memory), zeros for ranks at or past r
     int brow[Lay::NB], bcol[Lay::NB];
+    bool bval[Lay::NB];
 #pragma unroll
     for (int q = 0; q < Lay::NB; ++q) {
-        const int off = 1024 * (4 * q + wave) + 16 * lane;
-        brow[q] = off / slab_b;
-        bcol[q] = off - brow[q] * slab_b;
+        const int blk = 4 * q + wave;
+        const int off = 1024 * blk + 16 * lane;
+        brow[q] = off / Lay::PITCH;
+        const int lq = Lay::bswz(brow[q], (off % Lay::PITCH) / 16);
+        bcol[q] = 16 * lq;
+        bval[q] = blk < Lay::NBC && 8 * lq < r;
     }
 
     // M^T is a plain bitmap whatever the caller's layout.
@@ -186,11 +203,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + 8 * lc) : (const void*)zsrc, dst);
             }
         } else if (j < 16 + Lay::NB) {
-            // B rows k0 .. k0+63 are one contiguous block; every wave issues
-            // NB copies, those past the block go to the sink
+            // the swizzled B slab of rows k0 .. k0+63; every wave issues NB
+            // copies, those past the slab go to the sink
             const int q = j - 16, blk = 4 * q + wave;
-            const bool real = blk < nbcopies;
-            const bool ok = real && (!RAGGED || k0 + brow[q] < R);
+            const bool real = blk < Lay::NBC;
+            const bool ok = bval[q] && (!RAGGED || k0 + brow[q] < R);
             const void* src = (const uint8_t*)Bm + ((int64_t)k0 + brow[q]) * (2 * (int64_t)ldb) + bcol[q];
             copy16_to_lds(ok ? src : (const void*)zsrc, real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
         } else {
@@ -237,14 +254,14 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const int mb = i >> 1, nb = i & 1;
         acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
     };
+    // ranks 16c + 8h .. +7 of B row 32kb + pik; the slab holds zeros for
+    // ranks at or past r, so the read needs no per-lane test (a lane-dependent
+    // branch would split the loop body and undo its per-slot schedule)
     auto read_bfr = [&](const uint8_t* sb, int kb) {
+        const int k = 32 * kb + pik;
 #pragma unroll
-        for (int c = 0; c < RK; ++c) {
-            const int j0 = 16 * c + 8 * h;
-            u32x4 v = zero_u32x4();
-            if (j0 < r) v = *(const u32x4*)(sb + Lay::B + (32 * kb + pik) * slab_b + 2 * j0);
-            bfr[c] = as_bf16x8(v);
-        }
+        for (int c = 0; c < RK; ++c)
+            bfr[c] = *(const bf16x8*)(sb + Lay::B + k * Lay::PITCH + 16 * Lay::bswz(k, 2 * c + h));
     };
     auto read_mw = [&](const uint8_t* sb) {
 #pragma unroll
