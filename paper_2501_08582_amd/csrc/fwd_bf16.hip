@@ -27,11 +27,22 @@
 // sub-step of stage kt+1 with its MFMAs; the remaining copies of that stage
 // go out in the merge slots of the next K-step's sub-step 0, still a K-step
 // ahead of the barrier that waits for them.  A wave stalls on a burst of
-// asynchronous copies, so spreading them keeps the matrix pipe fed.  X, W, A and mask slabs travel HBM -> LDS with
-// global_load_lds; accumulators (256 x 64 per wave) live in AGPRs.
+// asynchronous copies, so spreading them keeps the matrix pipe fed.  X, W, A
+// and mask slabs travel HBM -> LDS with global_load_lds; accumulators
+// (256 x 64 per wave) live in AGPRs.
+//
+// Folded merge (FOLD, for a scale s that is a power of two): s.B is then
+// exact in bf16, so the resident B operand is pre-scaled and the rank-r MFMA
+// accumulates onto W itself -- its accumulator starts as the W values of the
+// two sub-steps of a k half, unpacked to fp32 -- and a merge piece is only the
+// rounding and the select.  W + s.B.A is still formed in fp32 and rounded
+// once (the terms are added in another order).  The W slab rows a wave
+// unpacks are the rows its own copies fill, so the next stage's W is read
+// before the barrier, as soon as the wave's own W copies have landed.
 #include "gemm_common.hpp"
 #include "kernels.hpp"
 
+#include <cmath>
 #include <type_traits>
 
 namespace lors {
@@ -63,12 +74,23 @@ struct Layout {
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
 
+// A^T slab (rank rows j of 64 k): chunk c of row j is stored at chunk
+// c ^ aswz(j).  The merge reads it with ds_read_b64_tr_b16, 32 lanes per pass
+// covering 4 consecutive rows x 4 chunks; rows j and j + 2 are 256 bytes
+// apart (the same banks), so their chunk sets must differ, which the XOR by
+// 4 on every other row pair does (the X/W slabs' row-pair XOR by 1 would
+// only swap chunks within the pair each row reads: a 2-way conflict).
+__device__ __forceinline__ int aswz(int row) { return ((row >> 1) & 1) << 2; }
+__device__ __forceinline__ int aslab_elem_off(int row, int col) {
+    return row * kRow64 + (((col >> 3) ^ aswz(row)) << 4) + ((col & 7) << 1);
+}
+
 // RAGGED: some tile reaches past L, R or C (copies then check every lane and
 // read the zero page outside the tensors); otherwise every slab row and
 // K-chunk is in range and copies use a uniform base plus fixed offsets.
 // PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
 // taken as zero and the product is added onto Y.  ldb: row stride of B.
-template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2>
+template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD>
 __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
@@ -121,6 +143,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
                         v[e >> 1] |= (j0 + e < r ? (uint32_t)src[e] : 0u) << ((e & 1) * 16);
                 }
             }
+            if constexpr (FOLD) {  // s.B, exact for a power-of-two s
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] = pack_bf16x2(s * __uint_as_float(v[e] << 16), s * __uint_as_float(v[e] & 0xFFFF0000u));
+            }
             bfr[nb][c] = as_bf16x8(v);
         }
     }
@@ -141,7 +168,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 #pragma unroll
     for (int q = 0; q < Lay::NAW; ++q) {
         const int row = 8 * (4 * q + wave) + (lane >> 3);
-        const int lc = (lane & 7) ^ ((row >> 1) & 7);
+        const int lc = (lane & 7) ^ aswz(row);
         aptr[q] = Am + (int64_t)row * C + 8 * lc;
     }
     // mask words [row n][kb]: two 256-byte copies per wave
@@ -177,7 +204,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             const int q = j - 16, blk = 4 * q + wave;
             const bool has = blk < 2 * RK;
             const int row = 8 * blk + (lane >> 3);
-            const int lc = (lane & 7) ^ ((row >> 1) & 7);
+            const int lc = (lane & 7) ^ aswz(row);
             const bool ok = has && row < r && (!RAGGED || k0 + 8 * lc < C);
             copy16_to_lds(ok ? (const void*)(aptr[q] + k0) : (const void*)zsrc,
                           has ? sb + Lay::A + 1024 * blk : lds0 + Lay::SINK);
@@ -208,7 +235,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             for (int t = 0; t < 2; ++t) {
                 const int row = 8 * (g >> 1) + 4 * t + (jj >> 2);
                 const int col = 32 * kb + 16 * (g & 1) + 4 * sig;
-                offAt[kb][t] = Lay::A + slab64_elem_off(row, col);
+                offAt[kb][t] = Lay::A + aslab_elem_off(row, col);
             }
     }
     const int nrow0 = 64 * wave + l32;
@@ -228,6 +255,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     f32x16 T[2];              // rank-r block of the current 32-wide k half
     uint32_t mw[2][2];        // mask words [nb][kb] of the current K-step
     u32x4 raw[2], sel[2];     // W and select masks of the sub-step being merged
+    u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
     bf16x8 afr[RK];
 
     auto mm = [&](int i, const bf16x8 (&xf)[8], const u32x4 (&wf)[2]) {
@@ -266,6 +294,28 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const int nb = p >> 2, q = p & 3;
         wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
     };
+    // folded merge: W of sub-step c4 (raw bf16 pairs), select masks of c4
+    auto read_raw = [&](u32x4 (&rw)[2], const uint8_t* sb, int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) rw[nb] = *(const u32x4*)(sb + woff(nb, c4));
+    };
+    auto read_sel = [&](int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
+            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+        }
+    };
+    // pair p of rw, as fp32, into the accumulator half cp of the rank-r block
+    auto unpack = [&](const u32x4 (&rw)[2], int cp, int p) {
+        const int nb = p >> 2, q = p & 3;
+        T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
+        T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+    };
+    auto merge_fold = [&](u32x4 (&wf)[2], int p, int cp) {
+        const int nb = p >> 2, q = p & 3;
+        wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
+    };
     // an ordinary sub-step: MFMAs on (xc, wc) while preparing (xn, wn) for
     // sub-step c4n of the stage at sb; optionally the rank-r block of k half 1
     // late_*: the copies kEarly.. of the stage in the other buffer, issued in
@@ -292,6 +342,50 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         if constexpr (RANK) rank_mfma2<RK>(T, afr, bfr);  // after the merge pieces read T
         SLOT_END();
     };
+    // The same sub-step with the folded merge.  The accumulator T holds, per
+    // k half, W + s.B.A of its two sub-steps (cp = 0, 1):
+    //   sub-step 1 (RANK): merges sub-step 1 from T's cp 1 and refills it, pair
+    //     by pair, with W of sub-step 3; W of sub-step 2 goes to cp 0 (free
+    //     since the previous K-step's last merge); then the rank-r MFMAs of
+    //     k half 1 accumulate onto both;
+    //   sub-step 2: merges sub-step 2 from cp 0;
+    //   sub-step 3: merges sub-step 3 from cp 1 and refills T with W of the
+    //     next stage's sub-steps 0 and 1, read once this wave's own W copies
+    //     of that stage have landed (no barrier needed: each wave copies the
+    //     W rows it merges); the rank-r MFMAs of that k half run after the
+    //     barrier.
+    auto substep_fold = [&](const bf16x8 (&xc)[8], const u32x4 (&wc)[2], bf16x8 (&xn)[8], u32x4 (&wn)[2],
+                            const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
+                            uint32_t late_sq = 0, bool late_on = false) {
+        const int cp = c4n & 1;
+        mm(0, xc, wc); read_sel(c4n); if (c4n == 1) read_raw(rwa, sb, 2); SLOT_END();
+        mm(1, xc, wc); if (c4n == 1) { read_afr(sb, 1); read_raw(rwb, sb, 3); } SLOT_END();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            mm(2 + i, xc, wc);
+            read_x2(xn, sb, c4n, i);
+            if (c4n == 1) { unpack(rwa, 0, 2 * i); unpack(rwa, 0, 2 * i + 1); }
+            if (c4n == 3 && i == 3) {
+                wait_vmcnt<Lay::NAW + 2>();  // this wave's W copies of the next stage
+                read_raw(rwa, snext, 0);
+                read_raw(rwb, snext, 1);
+            }
+            SLOT_END();
+        }
+        mm(6, xc, wc); SLOT_END();
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, xc, wc);
+            merge_fold(wn, p, cp);
+            if (c4n == 1) unpack(rwb, 1, p);
+            if (c4n == 3) { unpack(rwb, 1, p); unpack(rwa, 0, p); }
+            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            SLOT_END();
+        }
+        mm(15, xc, wc);
+        if (c4n == 1) rank_mfma2_acc<RK>(T, afr, bfr);  // after the merge pieces read T
+        SLOT_END();
+    };
 
     if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
         for (int i = tid; i < 2 * (WB / 16); i += NT)
@@ -307,12 +401,27 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     stage_barrier<0>();
     read_mw(smem);
     read_afr(smem, 0);
-    rank_mfma2<RK>(T, afr, bfr);
-    read_rs(smem, 0);
+    if constexpr (FOLD) {
+        read_raw(rwa, smem, 0);
+        read_raw(rwb, smem, 1);
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            unpack(rwa, 0, p);
+            unpack(rwb, 1, p);
+        }
+        rank_mfma2_acc<RK>(T, afr, bfr);
+        read_sel(0);
+    } else {
+        rank_mfma2<RK>(T, afr, bfr);
+        read_rs(smem, 0);
+    }
 #pragma unroll
     for (int p = 0; p < 4; ++p) read_x2(xa, smem, 0, p);
 #pragma unroll
-    for (int p = 0; p < 8; ++p) merge_piece(wa, p, 0);
+    for (int p = 0; p < 8; ++p) {
+        if constexpr (FOLD) merge_fold(wa, p, 0);
+        else merge_piece(wa, p, 0);
+    }
 
     // ---- main loop (no data-dependent branches: at the tail the copies
     // repeat the last K-slab into the buffer just consumed, and the reads of
@@ -325,9 +434,15 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         // barrier; the barrier below waits for them); at kt = 0 the prologue
         // issued all of stage 1
         const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
-        substep(xa, wa, xb, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
-        substep(xb, wb, xa, wa, sb, 2, std::false_type{});
-        substep(xa, wa, xb, wb, sb, 3, std::false_type{});
+        if constexpr (FOLD) {
+            substep_fold(xa, wa, xb, wb, sb, sn, 1, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
+            substep_fold(xb, wb, xa, wa, sb, sn, 2);
+            substep_fold(xa, wa, xb, wb, sb, sn, 3);
+        } else {
+            substep(xa, wa, xb, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
+            substep(xb, wb, xa, wa, sb, 2, std::false_type{});
+            substep(xa, wa, xb, wb, sb, 3, std::false_type{});
+        }
         // sub-step 3: stage kt+1 landed everywhere, stage kt free
         stage_barrier<0>();
         const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
@@ -338,13 +453,20 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         mm(1, xb, wb); copy_j(1, k2, sq); SLOT_END();
         mm(2, xb, wb); read_x2(xa, sn, 0, 0); copy_j(2, k2, sq); SLOT_END();
         mm(3, xb, wb); read_x2(xa, sn, 0, 1); copy_j(3, k2, sq); SLOT_END();
-        mm(4, xb, wb); read_rs(sn, 0); copy_j(4, k2, sq); SLOT_END();
+        mm(4, xb, wb);
+        if constexpr (FOLD) read_sel(0);
+        else read_rs(sn, 0);
+        copy_j(4, k2, sq); SLOT_END();
         mm(5, xb, wb); read_x2(xa, sn, 0, 2); copy_j(5, k2, sq); SLOT_END();
-        mm(6, xb, wb); read_x2(xa, sn, 0, 3); rank_mfma2<RK>(T, afr, bfr); copy_j(6, k2, sq); SLOT_END();
+        mm(6, xb, wb); read_x2(xa, sn, 0, 3);
+        if constexpr (FOLD) rank_mfma2_acc<RK>(T, afr, bfr);
+        else rank_mfma2<RK>(T, afr, bfr);
+        copy_j(6, k2, sq); SLOT_END();
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xb, wb);
-            merge_piece(wa, p, 0);
+            if constexpr (FOLD) merge_fold(wa, p, 0);
+            else merge_piece(wa, p, 0);
             if (7 + p < kEarly) copy_j(7 + p, k2, sq);
             SLOT_END();
         }
@@ -395,6 +517,14 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     }
 }
 
+// s.B is exact in bf16 for a power-of-two s (B's exponent shifts); the folded
+// merge needs that.
+bool power_of_two(float s) {
+    int e = 0;
+    const float m = std::frexp(s, &e);
+    return m == 0.5f || m == -0.5f;
+}
+
 template <int RK, bool TWO_FOUR, bool PASS2>
 hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
@@ -415,13 +545,18 @@ hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     // per-lane byte offsets (256 slab rows of C bf16 or of the mask) inside
     // 32 bits
     const bool ragged = a.L % BM != 0 || a.R % BN != 0 || a.C % BK != 0 || (int64_t)BM * a.C * 2 >= (1ll << 31);
+    // whole tiles with a power-of-two scale take the folded merge
     if (ragged)
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true, PASS2, false>), grid, block, 0, st, X, W, a.M, B, A, bias,
+                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
+                           part);
+    else if (power_of_two(a.scale))
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2, true>), grid, block, 0, st, X, W, a.M, B, A, bias,
+                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
                            part);
     else
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2>), grid, block, 0, st, X, W, a.M, B, A, bias, Y,
-                           a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
+        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2, false>), grid, block, 0, st, X, W, a.M, B, A, bias,
+                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
                            part);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && sp.split > 1)

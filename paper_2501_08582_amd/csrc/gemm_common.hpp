@@ -161,6 +161,34 @@ __device__ __forceinline__ void rank_mfma2(f32x16 (&T)[2], const bf16x8 (&a)[RK]
     }
 }
 
+// The same products accumulated onto T: T[nb] += sum over c of
+// mfma(a[c], b[nb][c]).  T is written by VALU instructions just before (it
+// holds W when the merge folds W into the matrix product), so each chain
+// starts with wait states that cover a VALU write -> matrix source-C read,
+// which the compiler cannot see through inline assembly.
+template <int RK>
+__device__ __forceinline__ void rank_mfma2_acc(f32x16 (&T)[2], const bf16x8 (&a)[RK], const bf16x8 (&b)[2][RK]) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        asm volatile("s_nop 4\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[0]), "v"(b[nb][0]));
+#pragma unroll
+        for (int c = 1; c < RK; ++c)
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[c]), "v"(b[nb][c]));
+    }
+    if constexpr (RK == 1)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]));
+    else if constexpr (RK == 2)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]));
+    else if constexpr (RK == 3)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
+    else {
+        static_assert(RK == 4, "ranks up to 64");
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2"
+                     : "+v"(T[0]), "+v"(T[1])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+    }
+}
+
 // One bf16 pair of W' = select(M, W + s.T, 0): raw holds the two bf16 of W,
 // t0/t1 the rank-r sums, sel the 32-bit select mask of the pair.
 __device__ __forceinline__ uint32_t merge_pair(uint32_t raw, float t0, float t1, float s, uint32_t sel) {

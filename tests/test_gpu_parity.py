@@ -714,3 +714,18 @@ def test_outputs_and_workspace_stay_in_bounds(R, C, L, r, mask, bias, split):
         assert np.all(np.isfinite(got)), f"{k}: an element was not written"
         e = relerr(got, ref)
         assert e <= TOL[dt], f"{k}: rel err {e:.3e}"
+
+
+# ---------------------------------------------------------------------------
+# scales: on whole tiles a power-of-two scale takes the folded merge (s.B is
+# exact in bf16, so the rank-r MFMA accumulates onto W), any other scale the
+# FMA merge; both must meet the bar, at every rank bucket of the kernels
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("scale", [1.0, -0.5, 0.25, 3.0, 0.1])
+@pytest.mark.parametrize("r,mask", [(16, "magnitude"), (48, "2:4"), (64, "magnitude"), (32, "2:4")])
+def test_parity_scales_whole_tiles(scale, r, mask):
+    name = "llama2_7b_up_proj_2_4" if mask == "2:4" else "llama2_7b_q_proj"
+    inp = _inputs(name, R=512, C=768, L=512, r=r, scale=scale, seed=3000 + r)
+    _check_all(inp)
+    if mask == "2:4" and r <= 64:
+        _check_all(inp, sparse_mfma=True)
