@@ -10,7 +10,9 @@
 // registers, in the B-operand layout of the main MFMA (rank-r MFMA with its
 // k rows taken in the order pi, see the forward kernel).  Differences:
 //   * W is stored [k][n] (k = R), so the raw W values a lane needs -- eight
-//     consecutive k of one column n -- come from two LDS transpose loads;
+//     consecutive k of one column n -- come from two LDS transpose loads; the
+//     W slab is four per-wave blocks (the 64 k rows of that wave's 64
+//     columns, tr64 layout), each filled by its own wave's copies;
 //   * the k-rows of the rank-r product are B[k][:], read from a B slab copied
 //     contiguously into LDS each K-step; A[:, n] is resident in registers;
 //   * the mask bits a lane needs run along k for a fixed n, so they are read
@@ -19,11 +21,16 @@
 // MFMA slot carrying a fixed share of the next sub-step's operand reads and
 // merge arithmetic, one barrier per K-step before the last sub-step, which
 // interleaves the copies of stage kt+2 and the first sub-step of stage kt+1.
+// For a power-of-two scale the merge is folded as in the forward: the
+// resident A operand is pre-scaled by s, the rank-r MFMA accumulates onto W
+// (read, for the next stage, as soon as the wave's own W copies landed), and
+// a merge piece is the rounding and the select.
 // Works on ranks that are multiples of 8, up to 64 per pass (the launcher pads
 // other ranks with a zero-filled copy of B and splits larger ones in two).
 #include "gemm_common.hpp"
 #include "kernels.hpp"
 
+#include <cmath>
 #include <type_traits>
 
 namespace lors {
@@ -37,7 +44,8 @@ constexpr int GROUP_M = 4;
 constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
 constexpr int DB = BM * kRow64;      // dY slab: 32 KiB
-constexpr int WB = BK * kRowBytes;   // W slab [k][n]: 32 KiB
+constexpr int WB = BK * kRowBytes;   // W slab: 4 per-wave blocks of [64 k][64 n], 32 KiB
+constexpr int WBW = WB / 4;          // one wave's block
 constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 
 // B slab [k][rank]: 64 rows of PITCH = 32*RKP bytes (ranks padded to 16*RKP;
@@ -74,7 +82,7 @@ struct Layout {
 // taken as zero and the product is added onto dX.  ldb: row stride of B.
 // r: the rank the kernel works on, a multiple of 8 (B's columns ra .. r-1
 // are zero); ra: the rows of A that exist (A rows ra .. r-1 are read as zero).
-template <int RK, bool RAGGED, bool PASS2>
+template <int RK, bool RAGGED, bool PASS2, bool FOLD>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
@@ -153,19 +161,31 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         for (int c = 0; c < RK; ++c)
             afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 0)),
                                       lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
+    if constexpr (FOLD) {  // s.A, exact for a power-of-two s
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int c = 0; c < RK; ++c) {
+                u32x4 v = __builtin_bit_cast(u32x4, afr[nb][c]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] = pack_bf16x2(s * __uint_as_float(v[e] << 16), s * __uint_as_float(v[e] & 0xFFFF0000u));
+                afr[nb][c] = as_bf16x8(v);
+            }
+    }
     lds_barrier();
 
     // ---- slab copies.  Copies 0..7: dY slab rows 8*(8*wave + q) + lane/8
-    // (64 k per row); copies 8..15: W slab rows 2*(8*wave + q) + h (256 n
-    // per row); then the B slab (one contiguous block) and the M^T words.
+    // (64 k per row); copies 8..15: rows 8q + lane/8 (k) of this wave's W
+    // block, its 64 columns; then the B slab and the M^T words.
     uint32_t offD[8], offW[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int blk = 8 * wave + q;
         const int rd = 8 * blk + (lane >> 3);
         offD[q] = (uint32_t)((rd * R + 8 * ((lane & 7) ^ ((rd >> 1) & 7))) * 2);
-        const int rw = 2 * blk + h;
-        offW[q] = (uint32_t)((rw * C + 8 * swz_chunk(rw, lane & 31)) * 2);
+        const int rw = 8 * q + (lane >> 3);
+        offW[q] = (uint32_t)((rw * C + 64 * wave + 8 * ((lane & 7) ^ tr64_swz(rw))) * 2);
     }
     uint32_t offM[2];
 #pragma unroll
@@ -192,15 +212,15 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             }
         } else if (j < 16) {
             if (PASS2) return;  // W is zero: its slabs were cleared once
-            const int q = j - 8, blk = 8 * wave + q;
-            const uint32_t dst = sb + Lay::W + 1024 * blk;
+            const int q = j - 8;
+            const uint32_t dst = sb + Lay::W + WBW * wave + 1024 * q;
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr(Wn + (int64_t)k0 * C), offW[q], dst);
             } else {
-                const int row = 2 * blk + h;
-                const int lc = swz_chunk(row, lane & 31);
-                const bool ok = k0 + row < R && n0 + 8 * lc < C;
-                copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + 8 * lc) : (const void*)zsrc, dst);
+                const int row = 8 * q + (lane >> 3);
+                const int col = 64 * wave + 8 * ((lane & 7) ^ tr64_swz(row));
+                const bool ok = k0 + row < R && n0 + col < C;
+                copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + col) : (const void*)zsrc, dst);
             }
         } else if (j < 16 + Lay::NB) {
             // the swizzled B slab of rows k0 .. k0+63; every wave issues NB
@@ -228,11 +248,19 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const int rho = l32;
     const int pik = 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho >> 3) & 1) + (rho & 3);
     const int ncol0 = 64 * wave + l32;
-    int offWt[2][2];  // transpose-read offsets of the raw W fragments, sub-step row 0
+    // transpose-read offsets of the raw W fragments in this wave's W block,
+    // sub-step 0 (sub-step c4 is 16 rows further): group g of 16 lanes reads
+    // rows 8(g/2) + 4t + 0..3, columns 32nb + 16(g%2) + 0..15
+    int offWt[2][2];
+    {
+        const int g = lane >> 4, jj = lane & 15;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) offWt[nb][t] = Lay::W + tr_frag_off(lane, 0, 64 * wave + 32 * nb, t);
+            for (int t = 0; t < 2; ++t)
+                offWt[nb][t] = Lay::W + WBW * wave +
+                               tr64_elem_off(8 * (g >> 1) + 4 * t + (jj >> 2), 32 * nb + 16 * (g & 1) + 4 * (jj & 3));
+    }
     auto doff = [&](int mb, int c4) { return Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h); };
 
     f32x16 acc[8][2];
@@ -248,6 +276,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     f32x16 T[2];              // rank-r block of the current 32-wide k half
     uint32_t mw[2][2];        // M^T words [nb][kb] of the current K-step
     u32x4 raw[2], sel[2];
+    u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
     bf16x8 bfr[RK];           // B[32kb + pi(rho)][16c + 8h .. +7]
 
     auto mm = [&](int i, const bf16x8 (&df)[8], const u32x4 (&wf)[2]) {
@@ -274,8 +303,8 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     auto read_rs = [&](const uint8_t* sb, int c4) {
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
-            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRowBytes);
-            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRowBytes);
+            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRow64);
+            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRow64);
             raw[nb][0] = lo[0];
             raw[nb][1] = lo[1];
             raw[nb][2] = hi[0];
@@ -291,6 +320,35 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
         wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
+    };
+    // folded merge (see the forward kernel): raw W of sub-step c4, its select
+    // masks, the unpack of a W pair into the rank-r accumulator, the merge
+    auto read_raw = [&](u32x4 (&rw)[2], const uint8_t* sb, int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRow64);
+            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRow64);
+            rw[nb][0] = lo[0];
+            rw[nb][1] = lo[1];
+            rw[nb][2] = hi[0];
+            rw[nb][3] = hi[1];
+        }
+    };
+    auto read_sel = [&](int c4) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
+            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+        }
+    };
+    auto unpack = [&](const u32x4 (&rw)[2], int cp, int p) {
+        const int nb = p >> 2, q = p & 3;
+        T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
+        T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+    };
+    auto merge_fold = [&](u32x4 (&wf)[2], int p, int cp) {
+        const int nb = p >> 2, q = p & 3;
+        wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
     };
     // late_*: the copies kEarly.. of the stage in the other buffer, issued in
     // the merge slots of the first sub-step of a K-step (see the main loop)
@@ -316,6 +374,39 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         if constexpr (RANK) rank_mfma2<RK>(T, bfr, afr);  // after the merge pieces read T
         SLOT_END();
     };
+    // the sub-steps with the folded merge (schedule as in the forward)
+    auto substep_fold = [&](const bf16x8 (&dc)[8], const u32x4 (&wc)[2], bf16x8 (&dn)[8], u32x4 (&wn)[2],
+                            const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
+                            uint32_t late_sq = 0, bool late_on = false) {
+        const int cp = c4n & 1;
+        mm(0, dc, wc); read_sel(c4n); if (c4n == 1) read_raw(rwa, sb, 2); SLOT_END();
+        mm(1, dc, wc); if (c4n == 1) { read_bfr(sb, 1); read_raw(rwb, sb, 3); } SLOT_END();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            mm(2 + i, dc, wc);
+            read_d2(dn, sb, c4n, i);
+            if (c4n == 1) { unpack(rwa, 0, 2 * i); unpack(rwa, 0, 2 * i + 1); }
+            if (c4n == 3 && i == 3) {
+                wait_vmcnt<Lay::NB + 2>();  // this wave's W copies of the next stage
+                read_raw(rwa, snext, 0);
+                read_raw(rwb, snext, 1);
+            }
+            SLOT_END();
+        }
+        mm(6, dc, wc); SLOT_END();
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            mm(7 + p, dc, wc);
+            merge_fold(wn, p, cp);
+            if (c4n == 1) unpack(rwb, 1, p);
+            if (c4n == 3) { unpack(rwb, 1, p); unpack(rwa, 0, p); }
+            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            SLOT_END();
+        }
+        mm(15, dc, wc);
+        if (c4n == 1) rank_mfma2_acc<RK>(T, bfr, afr);  // after the merge pieces read T
+        SLOT_END();
+    };
 
     if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
         for (int i = tid; i < 2 * (WB / 16); i += NT)
@@ -331,12 +422,27 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     stage_barrier<0>();
     read_mw(smem);
     read_bfr(smem, 0);
-    rank_mfma2<RK>(T, bfr, afr);
-    read_rs(smem, 0);
+    if constexpr (FOLD) {
+        read_raw(rwa, smem, 0);
+        read_raw(rwb, smem, 1);
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            unpack(rwa, 0, p);
+            unpack(rwb, 1, p);
+        }
+        rank_mfma2_acc<RK>(T, bfr, afr);
+        read_sel(0);
+    } else {
+        rank_mfma2<RK>(T, bfr, afr);
+        read_rs(smem, 0);
+    }
 #pragma unroll
     for (int p = 0; p < 4; ++p) read_d2(da, smem, 0, p);
 #pragma unroll
-    for (int p = 0; p < 8; ++p) merge_piece(wa, p, 0);
+    for (int p = 0; p < 8; ++p) {
+        if constexpr (FOLD) merge_fold(wa, p, 0);
+        else merge_piece(wa, p, 0);
+    }
 
     // ---- main loop (branch-free, see the forward kernel)
     for (int kt = 0; kt < nk; ++kt) {
@@ -347,9 +453,15 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         // barrier; the barrier below waits for them); at kt = 0 the prologue
         // issued all of stage 1
         const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
-        substep(da, wa, db, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
-        substep(db, wb, da, wa, sb, 2, std::false_type{});
-        substep(da, wa, db, wb, sb, 3, std::false_type{});
+        if constexpr (FOLD) {
+            substep_fold(da, wa, db, wb, sb, sn, 1, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
+            substep_fold(db, wb, da, wa, sb, sn, 2);
+            substep_fold(da, wa, db, wb, sb, sn, 3);
+        } else {
+            substep(da, wa, db, wb, sb, 1, std::true_type{}, k1, lds0 + (st ^ 1) * Lay::STAGE, kt > 0);
+            substep(db, wb, da, wa, sb, 2, std::false_type{});
+            substep(da, wa, db, wb, sb, 3, std::false_type{});
+        }
         stage_barrier<0>();
         const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
         const uint32_t sq = lds0 + st * Lay::STAGE;
@@ -359,13 +471,20 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         mm(1, db, wb); copy_j(1, k2, sq); SLOT_END();
         mm(2, db, wb); read_d2(da, sn, 0, 0); copy_j(2, k2, sq); SLOT_END();
         mm(3, db, wb); read_d2(da, sn, 0, 1); copy_j(3, k2, sq); SLOT_END();
-        mm(4, db, wb); read_rs(sn, 0); copy_j(4, k2, sq); SLOT_END();
+        mm(4, db, wb);
+        if constexpr (FOLD) read_sel(0);
+        else read_rs(sn, 0);
+        copy_j(4, k2, sq); SLOT_END();
         mm(5, db, wb); read_d2(da, sn, 0, 2); copy_j(5, k2, sq); SLOT_END();
-        mm(6, db, wb); read_d2(da, sn, 0, 3); rank_mfma2<RK>(T, bfr, afr); copy_j(6, k2, sq); SLOT_END();
+        mm(6, db, wb); read_d2(da, sn, 0, 3);
+        if constexpr (FOLD) rank_mfma2_acc<RK>(T, bfr, afr);
+        else rank_mfma2<RK>(T, bfr, afr);
+        copy_j(6, k2, sq); SLOT_END();
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, db, wb);
-            merge_piece(wa, p, 0);
+            if constexpr (FOLD) merge_fold(wa, p, 0);
+            else merge_piece(wa, p, 0);
             if (7 + p < kEarly) copy_j(7 + p, k2, sq);
             SLOT_END();
         }
@@ -413,6 +532,13 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     }
 }
 
+// s.A is exact in bf16 for a power-of-two s; the folded merge needs that
+bool power_of_two(float s) {
+    int e = 0;
+    const float m = std::frexp(s, &e);
+    return m == 0.5f || m == -0.5f;
+}
+
 template <int RK, bool PASS2>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool clear) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
@@ -438,14 +564,19 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool c
     float* z0 = clear ? a.dB : nullptr;
     float* z1 = clear ? a.dA : nullptr;
     const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
+    // whole tiles with a power-of-two scale take the folded merge
     if (ragged)
-        hipLaunchKernelGGL((dx_kernel<RK, true, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, sp.n_full,
-                           sp.split, part);
+        hipLaunchKernelGGL((dx_kernel<RK, true, PASS2, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
+                           sp.n_full, sp.split, part);
+    else if (power_of_two(a.scale))
+        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2, true>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
+                           sp.n_full, sp.split, part);
     else
-        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L, (int)a.R,
-                           (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, sp.n_full,
-                           sp.split, part);
+        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
+                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
+                           sp.n_full, sp.split, part);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && sp.split > 1)
         e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.C, nullptr,

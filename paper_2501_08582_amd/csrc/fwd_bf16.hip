@@ -74,16 +74,10 @@ struct Layout {
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
 
-// A^T slab (rank rows j of 64 k): chunk c of row j is stored at chunk
-// c ^ aswz(j).  The merge reads it with ds_read_b64_tr_b16, 32 lanes per pass
-// covering 4 consecutive rows x 4 chunks; rows j and j + 2 are 256 bytes
-// apart (the same banks), so their chunk sets must differ, which the XOR by
-// 4 on every other row pair does (the X/W slabs' row-pair XOR by 1 would
-// only swap chunks within the pair each row reads: a 2-way conflict).
-__device__ __forceinline__ int aswz(int row) { return ((row >> 1) & 1) << 2; }
-__device__ __forceinline__ int aslab_elem_off(int row, int col) {
-    return row * kRow64 + (((col >> 3) ^ aswz(row)) << 4) + ((col & 7) << 1);
-}
+// A^T slab (rank rows j of 64 k) in the tr64 layout: chunk c of row j is
+// stored at chunk c ^ tr64_swz(j), because the merge reads it with transposed
+// 4-row fragments (the X/W slabs' row-pair XOR would leave those reads 2-way
+// conflicted).
 
 // RAGGED: some tile reaches past L, R or C (copies then check every lane and
 // read the zero page outside the tensors); otherwise every slab row and
@@ -168,7 +162,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 #pragma unroll
     for (int q = 0; q < Lay::NAW; ++q) {
         const int row = 8 * (4 * q + wave) + (lane >> 3);
-        const int lc = (lane & 7) ^ aswz(row);
+        const int lc = (lane & 7) ^ tr64_swz(row);
         aptr[q] = Am + (int64_t)row * C + 8 * lc;
     }
     // mask words [row n][kb]: two 256-byte copies per wave
@@ -204,7 +198,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             const int q = j - 16, blk = 4 * q + wave;
             const bool has = blk < 2 * RK;
             const int row = 8 * blk + (lane >> 3);
-            const int lc = (lane & 7) ^ aswz(row);
+            const int lc = (lane & 7) ^ tr64_swz(row);
             const bool ok = has && row < r && (!RAGGED || k0 + 8 * lc < C);
             copy16_to_lds(ok ? (const void*)(aptr[q] + k0) : (const void*)zsrc,
                           has ? sb + Lay::A + 1024 * blk : lds0 + Lay::SINK);
@@ -235,7 +229,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             for (int t = 0; t < 2; ++t) {
                 const int row = 8 * (g >> 1) + 4 * t + (jj >> 2);
                 const int col = 32 * kb + 16 * (g & 1) + 4 * sig;
-                offAt[kb][t] = Lay::A + aslab_elem_off(row, col);
+                offAt[kb][t] = Lay::A + tr64_elem_off(row, col);
             }
     }
     const int nrow0 = 64 * wave + l32;

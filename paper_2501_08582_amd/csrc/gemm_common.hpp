@@ -67,6 +67,16 @@ __device__ __forceinline__ int slab64_elem_off(int row, int col) {
     return slab64_off(row, col >> 3) + ((col & 7) << 1);
 }
 
+// Slabs with 64 bf16 per row that are read as transposed 4-row fragments
+// (ds_read_b64_tr_b16): a 32-lane pass reads 4 consecutive rows x 4 chunks,
+// and rows j and j + 2 are 256 bytes apart, on the same banks.  Chunk c of
+// row j is therefore stored at c ^ tr64_swz(j), which gives every other row
+// pair the other 64-byte half and makes the pass conflict-free.
+__device__ __forceinline__ int tr64_swz(int row) { return ((row >> 1) & 1) << 2; }
+__device__ __forceinline__ int tr64_elem_off(int row, int col) {
+    return row * kRow64 + (((col >> 3) ^ tr64_swz(row)) << 4) + ((col & 7) << 1);
+}
+
 // Byte-to-select LUT: entry b holds four 32-bit AND masks, one per packed
 // bf16 pair (2p, 2p+1), keeping element q iff bit q of the 8 keep bits is set.
 // For the 2:4 layout the byte is two group codes and the keep bits are
