@@ -92,7 +92,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     using Lay = Layout<RK>;
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
     static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
-    static_assert(16 * RK * kRowBytes <= Lay::STAGE, "A block fits one stage");
+    static_assert(16 * RK * kRowBytes <= DB, "A block fits stage 1's dY region (clear of the W slabs)");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -142,38 +142,6 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     // M^T is a plain bitmap whatever the caller's layout.
     *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
 
-    // ---- prologue: A[:, n0 .. n0+255] (16*RK rows) -> stage 1, then the
-    // merge's B operand A[16c + 8h + e][n] into registers via transpose loads.
-#pragma unroll
-    for (int q = 0; q < 2 * RK; ++q) {
-        const int blk = 4 * q + wave;
-        const int row = 2 * blk + h;
-        const int lc = swz_chunk(row, lane & 31);
-        const int gn = n0 + 8 * lc;
-        copy16_to_lds((row < ra && gn < C) ? (const void*)(Am + (int64_t)row * C + gn) : (const void*)zsrc,
-                      lds0 + Lay::STAGE + 1024 * blk);
-    }
-    stage_barrier<0>();
-    bf16x8 afr[2][RK];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int c = 0; c < RK; ++c)
-            afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 0)),
-                                      lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
-    if constexpr (FOLD) {  // s.A, exact for a power-of-two s
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-            for (int c = 0; c < RK; ++c) {
-                u32x4 v = __builtin_bit_cast(u32x4, afr[nb][c]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = pack_bf16x2(s * __uint_as_float(v[e] << 16), s * __uint_as_float(v[e] & 0xFFFF0000u));
-                afr[nb][c] = as_bf16x8(v);
-            }
-    }
-    lds_barrier();
 
     // ---- slab copies.  Copies 0..7: dY slab rows 8*(8*wave + q) + lane/8
     // (64 k per row); copies 8..15: rows 8q + lane/8 (k) of this wave's W
@@ -278,6 +246,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     u32x4 raw[2], sel[2];
     u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
     bf16x8 bfr[RK];           // B[32kb + pi(rho)][16c + 8h .. +7]
+    bf16x8 afr[2][RK];        // A[16c + 8h .. +7][n] (scaled by s when the merge is folded)
 
     auto mm = [&](int i, const bf16x8 (&df)[8], const u32x4 (&wf)[2]) {
         const int mb = i >> 1, nb = i & 1;
@@ -414,12 +383,45 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         __syncthreads();
     }
 
-    // ---- prologue: stages 0 and 1 in flight, then sub-step 0 of stage 0
+    // ---- prologue.  The A block of the merge goes to stage 1's dY region
+    // while stage 0 is copied; once both landed, the A block is read into
+    // registers and stage 1 is copied over it (the first K-step's barrier
+    // waits for stage 1), so the two round trips to memory overlap.
+    // A[:, n0 .. n0+255] (16*RK rows) -> stage 1's dY region
+#pragma unroll
+    for (int q = 0; q < 2 * RK; ++q) {
+        const int blk = 4 * q + wave;
+        const int row = 2 * blk + h;
+        const int lc = swz_chunk(row, lane & 31);
+        const int gn = n0 + 8 * lc;
+        copy16_to_lds((row < ra && gn < C) ? (const void*)(Am + (int64_t)row * C + gn) : (const void*)zsrc,
+                      lds0 + Lay::STAGE + 1024 * blk);
+    }
 #pragma unroll
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
+    stage_barrier<0>();
+    // the merge's B operand A[16c + 8h + e][n] into registers via transpose loads
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int c = 0; c < RK; ++c)
+            afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 0)),
+                                      lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
+    if constexpr (FOLD) {  // s.A, exact for a power-of-two s
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int c = 0; c < RK; ++c) {
+                u32x4 v = __builtin_bit_cast(u32x4, afr[nb][c]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] = pack_bf16x2(s * __uint_as_float(v[e] << 16), s * __uint_as_float(v[e] & 0xFFFF0000u));
+                afr[nb][c] = as_bf16x8(v);
+            }
+    }
+    lds_barrier();
 #pragma unroll
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, nk > 1 ? BK : 0, lds0 + Lay::STAGE);
-    stage_barrier<0>();
     read_mw(smem);
     read_bfr(smem, 0);
     if constexpr (FOLD) {
