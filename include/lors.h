@@ -132,7 +132,12 @@ typedef enum lors_mask_format {
 
 /* Forward and backward calls: when the forward's or dX's grid of 256 x 256
  * output tiles ends in a partial wave that fills at most half of the GPU's
- * compute units (e.g. 320 tiles on 256 CUs), the tiles of that wave are cut
+ * compute units (e.g. 320 tiles on 256 CUs), that wave is spread over more
+ * CUs.  On shapes of whole tiles (L and the output features multiples of
+ * 256, the contraction a multiple of 64) this happens with or without the
+ * flag and needs no workspace: each tile of the wave is cut over its tokens
+ * into 2, 4 or 8 thin tiles, which compute the same bits as the whole tile.
+ * On other shapes, with this flag, the tiles of that wave are cut
  * along their contraction (K) into up to 8 pieces, one per CU.  Each piece
  * writes its fp32 partial sums (256 KiB) to the workspace; a small reduction
  * launch adds a tile's pieces in a fixed order, adds the bias and rounds

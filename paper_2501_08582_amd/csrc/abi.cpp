@@ -152,14 +152,16 @@ static int64_t split_budget(const lors_problem_t* p) {
 }
 // fp32 partial sums of the forward's or dX's split tiles (the larger of the
 // two; the calls run one after the other), with LORS_FLAG_SPLIT_LAST_WAVE.
+// Only shapes without whole tiles split over K: on whole-tile shapes the
+// same short waves run as thin tiles, which need no partials.
 static size_t split_bytes(const lors_problem_t* p) {
     if ((p->flags & LORS_FLAG_SPLIT_LAST_WAVE) == 0u || p->dtype != LORS_DTYPE_BF16 || p->L == 0) return 0;
     const int64_t tl = (p->L + 255) / 256;
     const int64_t budget = split_budget(p);
     int64_t fwd = 0, dx = 0;
-    if (p->r <= 64 && (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) == 0u)
+    if (p->r <= 64 && (p->flags & LORS_FLAG_FWD_SPARSE_MFMA) == 0u && !lors::fwd_whole_tiles(p->L, p->R, p->C))
         fwd = lors::split_part_bytes(lors::tail_split(tl * ((p->R + 255) / 256), (p->C + 63) / 64, budget));
-    if (padded_rank(p->r) <= 64)
+    if (padded_rank(p->r) <= 64 && !lors::dx_whole_tiles(p->L, p->R, p->C))
         dx = lors::split_part_bytes(lors::tail_split(tl * ((p->C + 255) / 256), (p->R + 63) / 64, budget));
     return static_cast<size_t>(fwd > dx ? fwd : dx);
 }

@@ -119,6 +119,26 @@ __device__ __forceinline__ void work_coords(int bid, int tiles_m, int tiles_n, i
     group_coords(t, tiles_m, tiles_n, group_m, tm, tn);
 }
 
+// Tile and sub-tile of a workgroup of a thin-tile grid (see thin_plan in
+// kernels.hpp): logical tiles first .. first+tail-1, in group_coords' order,
+// each cut over its tokens into q sub-tiles u = 0 .. q-1, one per id.  When
+// tail is a multiple of 8, the q sub-tiles of a tile get ids of one XCD (ids
+// are dealt to the 8 XCDs round-robin), so they share its weight slabs in
+// that XCD's L2.
+__device__ __forceinline__ void thin_coords(int bid, int tiles_m, int tiles_n, int group_m, int first, int tail,
+                                            int q, int& tm, int& tn, int& u) {
+    int i;
+    if ((tail & 7) == 0) {
+        const int x = bid & 7, y = bid >> 3;
+        u = y % q;
+        i = 8 * (y / q) + x;
+    } else {
+        i = bid / q;
+        u = bid - i * q;
+    }
+    group_coords(first + i, tiles_m, tiles_n, group_m, tm, tn);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }

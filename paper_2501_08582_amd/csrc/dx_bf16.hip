@@ -43,7 +43,6 @@ constexpr int BK = 64;   // output features (rows of W) per K-step
 constexpr int GROUP_M = 4;
 constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
-constexpr int DB = BM * kRow64;      // dY slab: 32 KiB
 constexpr int WB = BK * kRowBytes;   // W slab: 4 per-wave blocks of [64 k][64 n], 32 KiB
 constexpr int WBW = WB / 4;          // one wave's block
 constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
@@ -55,8 +54,10 @@ constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 // apart those rows would fall on only 8 / RKP of the 16 bank groups; the XOR
 // spreads them over all 16 (a 256-byte bank window holds 8 / RKP rows, and
 // bswz takes 2*RKP distinct values over 16 consecutive rows).
-template <int RK>
+// TM: tokens per tile, BM or (thin tiles of a short last wave) 128, 64, 32
+template <int RK, int TM>
 struct Layout {
+    static constexpr int DB = TM * kRow64;         // dY slab: TM rows of 64 k
     static constexpr int RKP = RK == 3 ? 4 : RK;
     static constexpr int PITCH = 32 * RKP;
     static constexpr int BB = BK * PITCH;          // B slab: 2 KiB per 16 ranks
@@ -67,8 +68,10 @@ struct Layout {
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NBC = BB / 1024;          // 1 KiB copies per B slab
     static constexpr int NB = (NBC + 3) / 4;       // B-slab copies per wave
-    static constexpr int COPIES = 16 + NB + 2;     // copies per wave per stage
+    static constexpr int ND = TM / 32;             // dY-slab copies per wave
+    static constexpr int COPIES = ND + 8 + NB + 2; // copies per wave per stage
     static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
+    static_assert(COPIES >= kEarly, "every early copy slot has a copy");
     // physical chunk of logical chunk q in B-slab row k
     static __device__ __forceinline__ int bswz(int k, int q) { return q ^ ((k / (8 / RKP)) & (2 * RKP - 1)); }
 };
@@ -82,17 +85,24 @@ struct Layout {
 // taken as zero and the product is added onto dX.  ldb: row stride of B.
 // r: the rank the kernel works on, a multiple of 8 (B's columns ra .. r-1
 // are zero); ra: the rows of A that exist (A rows ra .. r-1 are read as zero).
-template <int RK, bool RAGGED, bool PASS2, bool FOLD>
+// TM < BM: a thin tile of TM tokens and BN features (whole-tile shapes only),
+// as in the forward kernel.
+template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
     int ra, float s, int tiles_m, int tiles_n, int ldb, float* __restrict__ z0, int64_t nz0,
     float* __restrict__ z1, int64_t nz1, int n_full, int split, float* __restrict__ part) {
-    using Lay = Layout<RK>;
+    using Lay = Layout<RK, TM>;
+    constexpr int MBW = TM / 32;  // 32-token blocks per wave
+    static_assert(TM == BM || (!RAGGED && !PASS2), "thin tiles: fixed-offset copies, one pass");
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
-    static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
-    static_assert(16 * RK * kRowBytes <= DB, "A block fits stage 1's dY region (clear of the W slabs)");
+    static_assert(4 * TM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
+    // the prologue parks the merge's A block in stage 1: in its dY region,
+    // clear of the W slabs that PASS2 zeroes once (a thin tile's dY region is
+    // smaller, but it has no second pass and may use the whole stage)
+    static_assert(16 * RK * kRowBytes <= (TM == BM ? Lay::DB : Lay::STAGE), "A block fits stage 1");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -113,11 +123,22 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     }
 
     // tile and K-steps: ids past n_full are pieces of split tiles (their
-    // partial sums go to `part`, see the epilogue)
+    // partial sums go to `part`, see the epilogue).  Thin tiles: the grid
+    // covers logical tiles n_full .. n_full+split-1, each cut into BM/TM
+    // (see thin_coords), with every K-step.
     int tm, tn;
     int kbeg, nk;
-    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (R + BK - 1) / BK, tm, tn, kbeg, nk);
-    const int64_t m0 = (int64_t)tm * BM;
+    int64_t m0;
+    if constexpr (TM == BM) {
+        work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (R + BK - 1) / BK, tm, tn, kbeg, nk);
+        m0 = (int64_t)tm * BM;
+    } else {
+        int u;
+        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, BM / TM, tm, tn, u);
+        kbeg = 0;
+        nk = (R + BK - 1) / BK;
+        m0 = (int64_t)tm * BM + (int64_t)u * TM;
+    }
     const int n0 = tn * BN;
     const int kofs = kbeg * BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
@@ -143,15 +164,17 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
 
 
-    // ---- slab copies.  Copies 0..7: dY slab rows 8*(8*wave + q) + lane/8
-    // (64 k per row); copies 8..15: rows 8q + lane/8 (k) of this wave's W
+    // ---- slab copies.  Copies 0..ND-1: dY slab rows 8*(ND*wave + q) + lane/8
+    // (64 k per row); copies ND..ND+7: rows 8q + lane/8 (k) of this wave's W
     // block, its 64 columns; then the B slab and the M^T words.
-    uint32_t offD[8], offW[8];
+    uint32_t offD[Lay::ND], offW[8];
+#pragma unroll
+    for (int q = 0; q < Lay::ND; ++q) {
+        const int rd = 8 * (Lay::ND * wave + q) + (lane >> 3);
+        offD[q] = (uint32_t)((rd * R + 8 * ((lane & 7) ^ ((rd >> 1) & 7))) * 2);
+    }
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-        const int blk = 8 * wave + q;
-        const int rd = 8 * blk + (lane >> 3);
-        offD[q] = (uint32_t)((rd * R + 8 * ((lane & 7) ^ ((rd >> 1) & 7))) * 2);
         const int rw = 8 * q + (lane >> 3);
         offW[q] = (uint32_t)((rw * C + 64 * wave + 8 * ((lane & 7) ^ tr64_swz(rw))) * 2);
     }
@@ -167,8 +190,8 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 
     auto copy_j = [&](int j, int k0, uint32_t sb) {
         k0 += kofs;
-        if (j < 8) {
-            const int q = j, blk = 8 * wave + q;
+        if (j < Lay::ND) {
+            const int q = j, blk = Lay::ND * wave + q;
             const uint32_t dst = sb + Lay::D + 1024 * blk;
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr(Dt + k0), offD[q], dst);
@@ -178,9 +201,9 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 const bool ok = m0 + row < L && k0 + 8 * lc < R;
                 copy16_to_lds(ok ? (const void*)(Dt + (int64_t)row * R + k0 + 8 * lc) : (const void*)zsrc, dst);
             }
-        } else if (j < 16) {
+        } else if (j < Lay::ND + 8) {
             if (PASS2) return;  // W is zero: its slabs were cleared once
-            const int q = j - 8;
+            const int q = j - Lay::ND;
             const uint32_t dst = sb + Lay::W + WBW * wave + 1024 * q;
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr(Wn + (int64_t)k0 * C), offW[q], dst);
@@ -190,16 +213,16 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 const bool ok = k0 + row < R && n0 + col < C;
                 copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + col) : (const void*)zsrc, dst);
             }
-        } else if (j < 16 + Lay::NB) {
+        } else if (j < Lay::ND + 8 + Lay::NB) {
             // the swizzled B slab of rows k0 .. k0+63; every wave issues NB
             // copies, those past the slab go to the sink
-            const int q = j - 16, blk = 4 * q + wave;
+            const int q = j - Lay::ND - 8, blk = 4 * q + wave;
             const bool real = blk < Lay::NBC;
             const bool ok = bval[q] && (!RAGGED || k0 + brow[q] < R);
             const void* src = (const uint8_t*)Bm + ((int64_t)k0 + brow[q]) * (2 * (int64_t)ldb) + bcol[q];
             copy16_to_lds(ok ? src : (const void*)zsrc, real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
         } else {
-            const int q = j - 16 - Lay::NB;
+            const int q = j - Lay::ND - 8 - Lay::NB;
             const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
             if constexpr (!RAGGED) {
                 copy4s_to_lds(uniform_ptr(Mn + (k0 >> 5)), offM[q], dst);
@@ -231,15 +254,15 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     }
     auto doff = [&](int mb, int c4) { return Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h); };
 
-    f32x16 acc[8][2];
+    f32x16 acc[MBW][2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MBW; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    bf16x8 da[8], db[8];      // dY fragments of alternate sub-steps
+    bf16x8 da[MBW], db[MBW];  // dY fragments of alternate sub-steps
     u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
     f32x16 T[2];              // rank-r block of the current 32-wide k half
     uint32_t mw[2][2];        // M^T words [nb][kb] of the current K-step
@@ -248,9 +271,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     bf16x8 bfr[RK];           // B[32kb + pi(rho)][16c + 8h .. +7]
     bf16x8 afr[2][RK];        // A[16c + 8h .. +7][n] (scaled by s when the merge is folded)
 
-    auto mm = [&](int i, const bf16x8 (&df)[8], const u32x4 (&wf)[2]) {
+    // MFMA slot i of a sub-step: token block i/2, feature block i%2 (the
+    // slots of token blocks a thin tile lacks are empty)
+    auto mm = [&](int i, const bf16x8 (&df)[MBW], const u32x4 (&wf)[2]) {
         const int mb = i >> 1, nb = i & 1;
-        acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+        if (mb < MBW) acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
     };
     // ranks 16c + 8h .. +7 of B row 32kb + pik; the slab holds zeros for
     // ranks at or past r, so the read needs no per-lane test (a lane-dependent
@@ -282,9 +307,9 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
         }
     };
-    auto read_d2 = [&](bf16x8 (&df)[8], const uint8_t* sb, int c4, int p) {
-        df[2 * p] = *(const bf16x8*)(sb + doff(2 * p, c4));
-        df[2 * p + 1] = *(const bf16x8*)(sb + doff(2 * p + 1, c4));
+    auto read_d2 = [&](bf16x8 (&df)[MBW], const uint8_t* sb, int c4, int p) {
+        if (2 * p < MBW) df[2 * p] = *(const bf16x8*)(sb + doff(2 * p, c4));
+        if (2 * p + 1 < MBW) df[2 * p + 1] = *(const bf16x8*)(sb + doff(2 * p + 1, c4));
     };
     auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
@@ -321,7 +346,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     };
     // late_*: the copies kEarly.. of the stage in the other buffer, issued in
     // the merge slots of the first sub-step of a K-step (see the main loop)
-    auto substep = [&](const bf16x8 (&dc)[8], const u32x4 (&wc)[2], bf16x8 (&dn)[8], u32x4 (&wn)[2],
+    auto substep = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[2], bf16x8 (&dn)[MBW], u32x4 (&wn)[2],
                        const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
                        bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
@@ -344,7 +369,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         SLOT_END();
     };
     // the sub-steps with the folded merge (schedule as in the forward)
-    auto substep_fold = [&](const bf16x8 (&dc)[8], const u32x4 (&wc)[2], bf16x8 (&dn)[8], u32x4 (&wn)[2],
+    auto substep_fold = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[2], bf16x8 (&dn)[MBW], u32x4 (&wn)[2],
                             const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
                             uint32_t late_sq = 0, bool late_on = false) {
         const int cp = c4n & 1;
@@ -493,11 +518,11 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         mm(15, db, wb);
         SLOT_END();
     }
-    // ---- epilogue: round to bf16, stage the wave's 256 x 64 block in LDS
+    // ---- epilogue: round to bf16, stage the wave's TM x 64 block in LDS
     // (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
-    if ((int)blockIdx.x >= n_full) {
+    if (TM == BM && (int)blockIdx.x >= n_full) {
         // a piece of a split tile: its unrounded fp32 partial sums go to slice
         // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
         // reduction launch adds the pieces in order and rounds once
@@ -505,22 +530,22 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-            for (int mb = 0; mb < 8; ++mb)
+            for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + ncol0 + 32 * nb] = acc[mb][nb][v];
         return;
     }
-    uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
+    uint16_t* ol = (uint16_t*)(smem + wave * (TM * 128));
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
+        for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v]);
 #pragma unroll 4
-    for (int it = 0; it < BM / 8; ++it) {
+    for (int it = 0; it < TM / 8; ++it) {
         const int row = 8 * it + (lane >> 3), ch = lane & 7;
         const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
         const int64_t gm = m0 + row;
@@ -541,48 +566,62 @@ bool power_of_two(float s) {
     return m == 0.5f || m == -0.5f;
 }
 
+// z0, z1: dB (R x rank) and dA (rank x C) to clear, or null
+template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM>
+void launch_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, int grid, int tiles_m, int tiles_n, int n_full,
+               int split, float* part, float* z0, int64_t nz0, float* z1, int64_t nz1) {
+    hipLaunchKernelGGL((dx_kernel<RK, RAGGED, PASS2, FOLD, TM>), dim3(grid), dim3(NT), 0, st, (const uint16_t*)a.dY,
+                       (const uint16_t*)a.W, a.Mt, (const uint16_t*)a.B, (const uint16_t*)a.A, (uint16_t*)a.dX, a.L,
+                       (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, n_full,
+                       split, part);
+}
+
+#ifndef LORS_THIN_TILES
+
 template <int RK, bool PASS2>
 hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool clear) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.C + BN - 1) / BN);
-    // a partial last wave of tiles is cut over K when the caller gave room
-    // for the pieces' partial sums (one pass only: ranks up to 64)
-    TailSplit sp{tiles_m * tiles_n, 1, tiles_m * tiles_n};
-    if (a.split_ws != nullptr && !PASS2 && ldb <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.R + BK - 1) / BK, a.split_budget);
-    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
-    dim3 grid(sp.grid), block(NT);
+    const int tiles = tiles_m * tiles_n;
     // fixed-offset copies: whole tiles and K-steps, and per-lane byte
     // offsets (256 dY rows of R, 64 W rows of C, 256 M^T rows) inside 32 bits
-    const int64_t wprT = (a.R + 31) / 32;
-    const bool ragged = a.L % BM != 0 || a.C % BN != 0 || a.R % BK != 0 ||
-                        (int64_t)BM * a.R * 2 >= (1ll << 31) || (int64_t)BK * a.C * 2 >= (1ll << 31) ||
-                        (int64_t)BN * wprT * 4 >= (1ll << 31);
-    auto* dY = (const uint16_t*)a.dY;
-    auto* W = (const uint16_t*)a.W;
-    auto* B = (const uint16_t*)a.B;
-    auto* A = (const uint16_t*)a.A;
-    auto* dX = (uint16_t*)a.dX;
-    // clear: dB (R x rank) and dA (rank x C) of the caller's problem
-    float* z0 = clear ? a.dB : nullptr;
-    float* z1 = clear ? a.dA : nullptr;
-    const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
-    // whole tiles with a power-of-two scale take the folded merge
-    if (ragged)
-        hipLaunchKernelGGL((dx_kernel<RK, true, PASS2, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
-                           sp.n_full, sp.split, part);
-    else if (power_of_two(a.scale))
-        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2, true>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
-                           sp.n_full, sp.split, part);
-    else
-        hipLaunchKernelGGL((dx_kernel<RK, false, PASS2, false>), grid, block, 0, st, dY, W, a.Mt, B, A, dX, a.L,
-                           (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1,
-                           sp.n_full, sp.split, part);
+    const bool ragged = !dx_whole_tiles(a.L, a.R, a.C);
+    const bool fold = !ragged && power_of_two(a.scale);  // whole tiles with a power-of-two scale
+    // A short last wave on a whole-tile shape runs as thin tiles (the same
+    // bits, no workspace); on other shapes it is cut over K when the caller
+    // gave room for the pieces' partial sums (one pass only: ranks up to 64).
+    const ThinPlan tp = (!ragged && !PASS2) ? thin_plan(tiles) : ThinPlan{tiles, 0, 1};
+    TailSplit sp{tiles, 1, tiles};
+    if (tp.q == 1 && a.split_ws != nullptr && !PASS2 && ldb <= 64)
+        sp = tail_split(tiles, (a.R + BK - 1) / BK, a.split_budget);
+    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
+    // with thin tiles the whole-tile grid is exactly the first n_full tiles
+    // (work_coords regroups ids over the tiles it is told the grid holds)
+    const int grid = tp.q > 1 ? tp.n_full : sp.grid;
+    const int n_full = tp.q > 1 ? tp.n_full : sp.n_full;
+    // clear: dB (R x rank) and dA (rank x C) of the caller's problem, by the
+    // first launch of this call
+    const bool clear_here = clear && grid > 0;
+    float* z0 = clear_here ? a.dB : nullptr;
+    float* z1 = clear_here ? a.dA : nullptr;
+    const int64_t nz0 = clear_here ? a.R * a.r_grad : 0, nz1 = clear_here ? a.r_grad * a.C : 0;
+    if (grid > 0) {
+        if (ragged)
+            launch_tm<RK, true, PASS2, false, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
+                                                  nz0, z1, nz1);
+        else if (fold)
+            launch_tm<RK, false, PASS2, true, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
+                                                  nz0, z1, nz1);
+        else
+            launch_tm<RK, false, PASS2, false, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part,
+                                                   z0, nz0, z1, nz1);
+    }
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && tp.q > 1)
+        e = launch_dx_thin_bf16(a, st, ldb, ra, tp.n_full, tp.tail, tp.q, clear && !clear_here);
     if (e == hipSuccess && sp.split > 1)
         e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.C, nullptr,
-                                     dX, st);
+                                     a.dX, st);
     return e;
 }
 
@@ -599,7 +638,59 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb,
     }
 }
 
+#else  // LORS_THIN_TILES
+
+template <int RK, bool FOLD, int TM>
+hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, bool clear) {
+    const int tiles_m = (int)((a.L + BM - 1) / BM);
+    const int tiles_n = (int)((a.C + BN - 1) / BN);
+    float* z0 = clear ? a.dB : nullptr;
+    float* z1 = clear ? a.dA : nullptr;
+    const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
+    launch_tm<RK, false, false, FOLD, TM>(a, st, ldb, ra, tail * (BM / TM), tiles_m, tiles_n, first, tail, nullptr,
+                                          z0, nz0, z1, nz1);
+    return hipGetLastError();
+}
+
+template <int RK, bool FOLD>
+hipError_t launch_thin_q(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, int q,
+                         bool clear) {
+    switch (q) {
+        case 2: return launch_thin_tm<RK, FOLD, BM / 2>(a, st, ldb, ra, first, tail, clear);
+        case 4: return launch_thin_tm<RK, FOLD, BM / 4>(a, st, ldb, ra, first, tail, clear);
+        case 8: return launch_thin_tm<RK, FOLD, BM / 8>(a, st, ldb, ra, first, tail, clear);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int RK>
+hipError_t launch_thin_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, int q,
+                          bool clear) {
+    return power_of_two(a.scale) ? launch_thin_q<RK, true>(a, st, ldb, ra, first, tail, q, clear)
+                                 : launch_thin_q<RK, false>(a, st, ldb, ra, first, tail, q, clear);
+}
+
+#endif  // LORS_THIN_TILES
+
 }  // namespace
+
+#ifdef LORS_THIN_TILES
+
+hipError_t launch_dx_thin_bf16(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, int q,
+                               bool clear) {
+    if (tail <= 0) return hipSuccess;
+    // a.r: this pass's rank, a multiple of 8 up to 64 (see launch_dx_bf16)
+    if (!dx_whole_tiles(a.L, a.R, a.C) || a.r < 8 || a.r > 64 || a.r % 8 != 0) return hipErrorInvalidValue;
+    switch ((a.r + 15) / 16) {
+        case 1: return launch_thin_rk<1>(a, st, ldb, ra, first, tail, q, clear);
+        case 2: return launch_thin_rk<2>(a, st, ldb, ra, first, tail, q, clear);
+        case 3: return launch_thin_rk<3>(a, st, ldb, ra, first, tail, q, clear);
+        case 4: return launch_thin_rk<4>(a, st, ldb, ra, first, tail, q, clear);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+#else
 
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0 || a.dX == nullptr) return hipSuccess;
@@ -630,5 +721,7 @@ hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t st) {
     a2.A = (const uint16_t*)a.A + 64 * a.C;
     return launch_ranks(a2, st, true, rp, (int)a.r - 64);
 }
+
+#endif  // LORS_THIN_TILES
 
 }  // namespace lors

@@ -55,21 +55,24 @@ constexpr int BK = 64;    // input features per K-step
 constexpr int GROUP_M = 4;
 constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
-constexpr int XB = BM * kRow64;  // 32 KiB
 constexpr int WB = BN * kRow64;  // 32 KiB
 constexpr int MB = BN * 2 * 4;   // 2 mask words per row of W: 2 KiB
 
-template <int RK>
+// TM: tokens per tile, BM or (thin tiles of a short last wave) 128, 64, 32
+template <int RK, int TM>
 struct Layout {
+    static constexpr int XB = TM * kRow64;        // X slab: TM rows of 64 k
     static constexpr int AB = 16 * RK * kRow64;   // A slab: 16*RK rows of 64 k
     static constexpr int X = 0, W = XB, A = XB + WB, M = XB + WB + AB;
     static constexpr int STAGE = XB + WB + AB + MB;
     static constexpr int LUT = 2 * STAGE;         // 256 x 16 B
     static constexpr int SINK = LUT + 4096;       // 1 KiB target of padding copies
     static constexpr int TOTAL = SINK + 1024;
+    static constexpr int NX = TM / 32;            // X-slab copies per wave
     static constexpr int NAW = (2 * RK + 3) / 4;  // A-slab copies per wave
-    static constexpr int COPIES = 16 + NAW + 2;   // copies per wave per stage
+    static constexpr int COPIES = NX + 8 + NAW + 2;  // copies per wave per stage
     static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
+    static_assert(COPIES >= kEarly, "every early copy slot has a copy");
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -84,16 +87,21 @@ struct Layout {
 // K-chunk is in range and copies use a uniform base plus fixed offsets.
 // PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
 // taken as zero and the product is added onto Y.  ldb: row stride of B.
-template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD>
+// TM < BM: a thin tile of TM tokens and BN features (whole-tile shapes only);
+// each wave then holds TM x 64 accumulators and the MFMA slots and X reads
+// of the missing token blocks drop out of the schedule.
+template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD, int TM>
 __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, const uint16_t* __restrict__ bias,
     uint16_t* __restrict__ Y, int64_t L, int R, int C, int r, float s, int tiles_m,
     int tiles_n, int ldb, int n_full, int split, float* __restrict__ part) {
-    using Lay = Layout<RK>;
+    using Lay = Layout<RK, TM>;
+    constexpr int MBW = TM / 32;  // 32-token blocks per wave
+    static_assert(TM == BM || !RAGGED, "thin tiles take the fixed-offset copies");
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
-    static_assert(4 * BM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
+    static_assert(4 * TM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -103,11 +111,22 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const int h = lane >> 5;
 
     // tile and K-steps: ids past n_full are pieces of split tiles (their
-    // partial sums go to `part`, see the epilogue)
+    // partial sums go to `part`, see the epilogue).  Thin tiles: the grid
+    // covers logical tiles n_full .. n_full+split-1, each cut into BM/TM
+    // (see thin_coords), with every K-step.
     int tm, tn;
     int kbeg, nk;
-    work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg, nk);
-    const int64_t m0 = (int64_t)tm * BM;
+    int64_t m0;
+    if constexpr (TM == BM) {
+        work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg, nk);
+        m0 = (int64_t)tm * BM;
+    } else {
+        int u;
+        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, BM / TM, tm, tn, u);
+        kbeg = 0;
+        nk = (C + BK - 1) / BK;
+        m0 = (int64_t)tm * BM + (int64_t)u * TM;
+    }
     const int n0 = tn * BN;
     const int kofs = kbeg * BK;
     const int wpr = (C + 31) >> 5;
@@ -146,15 +165,22 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         }
     }
 
-    // ---- slab copies.  Copy q < 8 of a wave fills slab rows
-    // 8*(8*wave + q) + lane/8 of X (and, copies 8..15, of W); lane l covers
-    // physical chunk l % 8 of its row.  X and W slabs share the offsets.
-    uint32_t offXW[8];
+    // ---- slab copies.  Copy q < NX of a wave fills X slab rows
+    // 8*(NX*wave + q) + lane/8, copy NX + q (q < 8) W slab rows
+    // 8*(8*wave + q) + lane/8; lane l covers physical chunk l % 8 of its row.
+    // (With whole tiles NX = 8 and the two share their offsets.)
+    uint32_t offX[Lay::NX], offW[8];
+#pragma unroll
+    for (int q = 0; q < Lay::NX; ++q) {
+        const int row = 8 * (Lay::NX * wave + q) + (lane >> 3);
+        const int lc = (lane & 7) ^ ((row >> 1) & 7);
+        offX[q] = (uint32_t)((row * C + 8 * lc) * 2);
+    }
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int row = 8 * (8 * wave + q) + (lane >> 3);
         const int lc = (lane & 7) ^ ((row >> 1) & 7);
-        offXW[q] = (uint32_t)((row * C + 8 * lc) * 2);
+        offW[q] = (uint32_t)((row * C + 8 * lc) * 2);
     }
     // A slab: copy q of wave w is slab block 4q + w (rows 8 blk .. +7) when
     // that block exists; rows at or past r read zeros
@@ -179,23 +205,24 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // copy j of the stage at K offset k0 into the stage at LDS address sb
     auto copy_j = [&](int j, int k0, uint32_t sb) {
         k0 += kofs;
-        if (j < 16) {
-            const int q = j & 7;
-            const bool isx = j < 8;
+        if (j < Lay::NX + 8) {
+            const bool isx = j < Lay::NX;
+            const int q = isx ? j : j - Lay::NX;
             if (PASS2 && !isx) return;  // W is zero: its slabs were cleared once
-            const uint32_t dst = sb + (isx ? Lay::X : Lay::W) + 1024 * (8 * wave + q);
+            const int blk = isx ? Lay::NX * wave + q : 8 * wave + q;
+            const uint32_t dst = sb + (isx ? Lay::X : Lay::W) + 1024 * blk;
             if constexpr (!RAGGED) {
-                copy16s_to_lds(uniform_ptr((isx ? Xt : Wt) + k0), offXW[q], dst);
+                copy16s_to_lds(uniform_ptr((isx ? Xt : Wt) + k0), isx ? offX[q] : offW[q], dst);
             } else {
-                const int row = 8 * (8 * wave + q) + (lane >> 3);
+                const int row = 8 * blk + (lane >> 3);
                 const int lc = (lane & 7) ^ ((row >> 1) & 7);
                 const bool ok = (isx ? m0 + row < L : n0 + row < R) && k0 + 8 * lc < C;
                 const uint16_t* src = (isx ? Xt : Wt) + (int64_t)row * C + k0 + 8 * lc;
                 copy16_to_lds(ok ? (const void*)src : (const void*)zsrc, dst);
             }
-        } else if (j < 16 + Lay::NAW) {
+        } else if (j < Lay::NX + 8 + Lay::NAW) {
             // every wave issues NAW copies; those past the A slab go to the sink
-            const int q = j - 16, blk = 4 * q + wave;
+            const int q = j - Lay::NX - 8, blk = 4 * q + wave;
             const bool has = blk < 2 * RK;
             const int row = 8 * blk + (lane >> 3);
             const int lc = (lane & 7) ^ tr64_swz(row);
@@ -203,7 +230,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             copy16_to_lds(ok ? (const void*)(aptr[q] + k0) : (const void*)zsrc,
                           has ? sb + Lay::A + 1024 * blk : lds0 + Lay::SINK);
         } else {
-            const int q = j - 16 - Lay::NAW;
+            const int q = j - Lay::NX - 8 - Lay::NAW;
             const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
             if constexpr (!RAGGED) {
                 copy4s_to_lds(uniform_ptr(Mt + (k0 >> 5)), offM[q], dst);
@@ -236,15 +263,15 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     auto xoff = [&](int mb, int c4) { return Lay::X + slab64_off(32 * mb + l32, 2 * c4 + h); };
     auto woff = [&](int nb, int c4) { return Lay::W + slab64_off(nrow0 + 32 * nb, 2 * c4 + h); };
 
-    f32x16 acc[8][2];
+    f32x16 acc[MBW][2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MBW; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    bf16x8 xa[8], xb[8];      // X fragments of alternate sub-steps
+    bf16x8 xa[MBW], xb[MBW];  // X fragments of alternate sub-steps
     u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
     f32x16 T[2];              // rank-r block of the current 32-wide k half
     uint32_t mw[2][2];        // mask words [nb][kb] of the current K-step
@@ -252,9 +279,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
     bf16x8 afr[RK];
 
-    auto mm = [&](int i, const bf16x8 (&xf)[8], const u32x4 (&wf)[2]) {
+    // MFMA slot i of a sub-step: token block i/2, feature block i%2 (the
+    // slots of token blocks a thin tile lacks are empty)
+    auto mm = [&](int i, const bf16x8 (&xf)[MBW], const u32x4 (&wf)[2]) {
         const int mb = i >> 1, nb = i & 1;
-        acc[mb][nb] = mfma_32x32x16(xf[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+        if (mb < MBW) acc[mb][nb] = mfma_32x32x16(xf[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
     };
     auto read_afr = [&](const uint8_t* sb, int kb) {
 #pragma unroll
@@ -279,9 +308,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
         }
     };
-    auto read_x2 = [&](bf16x8 (&xf)[8], const uint8_t* sb, int c4, int p) {
-        xf[2 * p] = *(const bf16x8*)(sb + xoff(2 * p, c4));
-        xf[2 * p + 1] = *(const bf16x8*)(sb + xoff(2 * p + 1, c4));
+    auto read_x2 = [&](bf16x8 (&xf)[MBW], const uint8_t* sb, int c4, int p) {
+        if (2 * p < MBW) xf[2 * p] = *(const bf16x8*)(sb + xoff(2 * p, c4));
+        if (2 * p + 1 < MBW) xf[2 * p + 1] = *(const bf16x8*)(sb + xoff(2 * p + 1, c4));
     };
     // merge piece p (0..7): pair p % 4 of fragment nb = p / 4, T half cp
     auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
@@ -314,7 +343,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // sub-step c4n of the stage at sb; optionally the rank-r block of k half 1
     // late_*: the copies kEarly.. of the stage in the other buffer, issued in
     // the merge slots of the first sub-step of a K-step (see the main loop)
-    auto substep = [&](const bf16x8 (&xc)[8], const u32x4 (&wc)[2], bf16x8 (&xn)[8], u32x4 (&wn)[2],
+    auto substep = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[2], bf16x8 (&xn)[MBW], u32x4 (&wn)[2],
                        const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
                        bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
@@ -348,7 +377,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     //     of that stage have landed (no barrier needed: each wave copies the
     //     W rows it merges); the rank-r MFMAs of that k half run after the
     //     barrier.
-    auto substep_fold = [&](const bf16x8 (&xc)[8], const u32x4 (&wc)[2], bf16x8 (&xn)[8], u32x4 (&wn)[2],
+    auto substep_fold = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[2], bf16x8 (&xn)[MBW], u32x4 (&wn)[2],
                             const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
                             uint32_t late_sq = 0, bool late_on = false) {
         const int cp = c4n & 1;
@@ -467,11 +496,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         mm(15, xb, wb);
         SLOT_END();
     }
-    // ---- epilogue: (+bias), round to bf16, stage the wave's 256 x 64 block in
+    // ---- epilogue: (+bias), round to bf16, stage the wave's TM x 64 block in
     // LDS (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
-    if ((int)blockIdx.x >= n_full) {
+    if (TM == BM && (int)blockIdx.x >= n_full) {
         // a piece of a split tile: its unrounded fp32 partial sums go to slice
         // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
         // reduction launch adds the pieces in order, adds the bias and rounds
@@ -479,25 +508,25 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-            for (int mb = 0; mb < 8; ++mb)
+            for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + nrow0 + 32 * nb] = acc[mb][nb][v];
         return;
     }
-    uint16_t* ol = (uint16_t*)(smem + wave * (BM * 128));
+    uint16_t* ol = (uint16_t*)(smem + wave * (TM * 128));
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
         const int gn = n0 + nrow0 + 32 * nb;
         const float bv = (bias != nullptr && gn < R) ? bf16_bits_to_f32(bias[gn]) : 0.f;
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
+        for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v] + bv);
     }
 #pragma unroll 4
-    for (int it = 0; it < BM / 8; ++it) {
+    for (int it = 0; it < TM / 8; ++it) {
         const int row = 8 * it + (lane >> 3), ch = lane & 7;
         const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
         const int64_t gm = m0 + row;
@@ -519,42 +548,55 @@ bool power_of_two(float s) {
     return m == 0.5f || m == -0.5f;
 }
 
+#ifndef LORS_THIN_TILES
+
+template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD>
+void launch_whole(const LayerArgs& a, hipStream_t st, int ldb, int grid, int tiles_m, int tiles_n, int n_full,
+                  int split, float* part) {
+    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, RAGGED, PASS2, FOLD, BM>), dim3(grid), dim3(NT), 0, st,
+                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.M, (const uint16_t*)a.B,
+                       (const uint16_t*)a.A, (const uint16_t*)a.bias, (uint16_t*)a.Y, a.L, (int)a.R, (int)a.C,
+                       (int)a.r, a.scale, tiles_m, tiles_n, ldb, n_full, split, part);
+}
+
 template <int RK, bool TWO_FOUR, bool PASS2>
 hipError_t launch_fmt(const LayerArgs& a, hipStream_t st, int ldb) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.R + BN - 1) / BN);
-    // a partial last wave of tiles is cut over K when the caller gave room
-    // for the pieces' partial sums (one pass only: ranks up to 64)
-    TailSplit sp{tiles_m * tiles_n, 1, tiles_m * tiles_n};
-    if (a.split_ws != nullptr && !PASS2 && a.r <= 64) sp = tail_split((int64_t)tiles_m * tiles_n, (a.C + BK - 1) / BK, a.split_budget);
-    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
-    dim3 grid(sp.grid), block(NT);
-    auto* X = (const uint16_t*)a.X;
-    auto* W = (const uint16_t*)a.W;
-    auto* B = (const uint16_t*)a.B;
-    auto* A = (const uint16_t*)a.A;
-    auto* bias = (const uint16_t*)a.bias;
-    auto* Y = (uint16_t*)a.Y;
+    const int tiles = tiles_m * tiles_n;
     // the fixed-offset copies need every tile and K-step in range and the
     // per-lane byte offsets (256 slab rows of C bf16 or of the mask) inside
     // 32 bits
-    const bool ragged = a.L % BM != 0 || a.R % BN != 0 || a.C % BK != 0 || (int64_t)BM * a.C * 2 >= (1ll << 31);
-    // whole tiles with a power-of-two scale take the folded merge
-    if (ragged)
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, true, PASS2, false>), grid, block, 0, st, X, W, a.M, B, A, bias,
-                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
-                           part);
-    else if (power_of_two(a.scale))
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2, true>), grid, block, 0, st, X, W, a.M, B, A, bias,
-                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
-                           part);
-    else
-        hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, PASS2, false>), grid, block, 0, st, X, W, a.M, B, A, bias,
-                           Y, a.L, (int)a.R, (int)a.C, (int)a.r, a.scale, tiles_m, tiles_n, ldb, sp.n_full, sp.split,
-                           part);
+    const bool ragged = !fwd_whole_tiles(a.L, a.R, a.C);
+    const bool fold = !ragged && power_of_two(a.scale);  // whole tiles with a power-of-two scale
+    // A short last wave on a whole-tile shape runs as thin tiles (the same
+    // bits, no workspace); on other shapes it is cut over K when the caller
+    // gave room for the pieces' partial sums (one pass only: ranks up to 64).
+    const ThinPlan tp = (!ragged && !PASS2) ? thin_plan(tiles) : ThinPlan{tiles, 0, 1};
+    TailSplit sp{tiles, 1, tiles};
+    if (tp.q == 1 && a.split_ws != nullptr && !PASS2 && a.r <= 64)
+        sp = tail_split(tiles, (a.C + BK - 1) / BK, a.split_budget);
+    float* part = sp.split > 1 ? (float*)a.split_ws : nullptr;
+    // with thin tiles the whole-tile grid is exactly the first n_full tiles
+    // (work_coords regroups ids over the tiles it is told the grid holds)
+    const int grid = tp.q > 1 ? tp.n_full : sp.grid;
+    const int n_full = tp.q > 1 ? tp.n_full : sp.n_full;
+    if (grid > 0) {
+        if (ragged)
+            launch_whole<RK, TWO_FOUR, true, PASS2, false>(a, st, ldb, grid, tiles_m, tiles_n, n_full, sp.split,
+                                                           part);
+        else if (fold)
+            launch_whole<RK, TWO_FOUR, false, PASS2, true>(a, st, ldb, grid, tiles_m, tiles_n, n_full, sp.split,
+                                                           part);
+        else
+            launch_whole<RK, TWO_FOUR, false, PASS2, false>(a, st, ldb, grid, tiles_m, tiles_n, n_full, sp.split,
+                                                            part);
+    }
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && tp.q > 1) e = launch_fwd_thin_bf16(a, st, ldb, tp.n_full, tp.tail, tp.q);
     if (e == hipSuccess && sp.split > 1)
-        e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.R, bias, Y, st);
+        e = launch_split_reduce_bf16(part, sp.n_full, sp.split, tiles_m, tiles_n, GROUP_M, a.L, (int)a.R, a.bias,
+                                     a.Y, st);
     return e;
 }
 
@@ -575,7 +617,44 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb)
     }
 }
 
+#else  // LORS_THIN_TILES
+
+template <int RK, bool TWO_FOUR, bool FOLD, int TM>
+hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail) {
+    const int tiles_m = (int)((a.L + BM - 1) / BM);
+    const int tiles_n = (int)((a.R + BN - 1) / BN);
+    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, false, FOLD, TM>), dim3(tail * (BM / TM)), dim3(NT), 0, st,
+                       (const uint16_t*)a.X, (const uint16_t*)a.W, a.M, (const uint16_t*)a.B,
+                       (const uint16_t*)a.A, (const uint16_t*)a.bias, (uint16_t*)a.Y, a.L, (int)a.R, (int)a.C,
+                       (int)a.r, a.scale, tiles_m, tiles_n, ldb, first, tail, (float*)nullptr);
+    return hipGetLastError();
+}
+
+template <int RK, bool TWO_FOUR, bool FOLD>
+hipError_t launch_thin_q(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail, int q) {
+    switch (q) {
+        case 2: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 2>(a, st, ldb, first, tail);
+        case 4: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 4>(a, st, ldb, first, tail);
+        case 8: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 8>(a, st, ldb, first, tail);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int RK>
+hipError_t launch_thin_rk(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail, int q) {
+    const bool fold = power_of_two(a.scale);
+    if (a.two_four)
+        return fold ? launch_thin_q<RK, true, true>(a, st, ldb, first, tail, q)
+                    : launch_thin_q<RK, true, false>(a, st, ldb, first, tail, q);
+    return fold ? launch_thin_q<RK, false, true>(a, st, ldb, first, tail, q)
+                : launch_thin_q<RK, false, false>(a, st, ldb, first, tail, q);
+}
+
+#endif  // LORS_THIN_TILES
+
 }  // namespace
+
+#ifndef LORS_THIN_TILES
 
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t st) {
     if (a.L == 0) return hipSuccess;
@@ -597,5 +676,21 @@ hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t st) {
     a2.bias = nullptr;
     return launch_ranks(a2, st, true, (int)a.r);
 }
+
+#else
+
+hipError_t launch_fwd_thin_bf16(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail, int q) {
+    if (tail <= 0) return hipSuccess;
+    if (!fwd_whole_tiles(a.L, a.R, a.C) || a.r < 1 || a.r > 64) return hipErrorInvalidValue;
+    switch ((a.r + 15) / 16) {
+        case 1: return launch_thin_rk<1>(a, st, ldb, first, tail, q);
+        case 2: return launch_thin_rk<2>(a, st, ldb, first, tail, q);
+        case 3: return launch_thin_rk<3>(a, st, ldb, first, tail, q);
+        case 4: return launch_thin_rk<4>(a, st, ldb, first, tail, q);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+#endif  // LORS_THIN_TILES
 
 }  // namespace lors

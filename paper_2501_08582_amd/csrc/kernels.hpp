@@ -53,6 +53,31 @@ TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes);
 inline int64_t split_part_bytes(const TailSplit& t) {
     return t.split > 1 ? (int64_t)(t.grid - t.n_full) * kPieceBytes : 0;
 }
+// A short last wave of 256 x 256 tiles cut over its tokens instead: each of
+// its `tail` tiles becomes q thin tiles of 256/q tokens and all 256 output
+// features (q = 2, 4 or 8, as many as fill the CUs; q = 1: not cut).  A thin
+// tile runs the whole K-loop with the same per-element arithmetic as a whole
+// tile, so its results are the same bits, and it needs no workspace; it
+// merges the same W' rows, so a thin tile costs more than 1/q of a whole one.
+// Applies to a wave that fills at most half of the CUs, like tail_split.
+// n_full: the tiles that run whole (the first n_full in the kernels' order).
+struct ThinPlan {
+    int n_full, tail, q;
+};
+ThinPlan thin_plan(int64_t tiles);
+// Whether the forward (Y = X.W'^T, tiles over L x R, K = C) and the dX kernel
+// (dX = dY.W', tiles over L x C, K = R) take their fixed-offset copies: whole
+// 256 x 256 tiles and 64-wide K-steps, and per-lane byte offsets of 256 slab
+// rows inside 32 bits.  Thin tiles need them; other shapes run whole tiles
+// whose copies check every lane.
+inline bool fwd_whole_tiles(int64_t L, int64_t R, int64_t C) {
+    return L % 256 == 0 && R % 256 == 0 && C % 64 == 0 && 256 * C * 2 < (1ll << 31);
+}
+inline bool dx_whole_tiles(int64_t L, int64_t R, int64_t C) {
+    const int64_t wprT = (R + 31) / 32;
+    return L % 256 == 0 && C % 256 == 0 && R % 64 == 0 && 256 * R * 2 < (1ll << 31) && 64 * C * 2 < (1ll << 31) &&
+           256 * wprT * 4 < (1ll << 31);
+}
 // out (rows x cols, bf16) on the split tiles = the sum of their pieces'
 // partials in piece order (+ bias[col] when bias is not null), rounded once.
 // Tile coordinates follow work_coords with the same tiles_m, tiles_n, group_m.
@@ -64,6 +89,13 @@ hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, in
 hipError_t launch_fwd_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_fwd24_bf16(const LayerArgs& a, hipStream_t s);      // 2:4 mask, sparse MFMA, rank <= 64
 hipError_t launch_dx_bf16(const LayerArgs& a, hipStream_t s);
+// The thin tiles of a short last wave (see ThinPlan): logical tiles first ..
+// first+tail-1, each cut into q; single-pass ranks (a.r <= 64), whole-tile
+// shapes.  ldb: row stride of B; ra: rows of A that exist; clear: the launch
+// also clears dB and dA (it is the first of the dX launches).
+hipError_t launch_fwd_thin_bf16(const LayerArgs& a, hipStream_t s, int ldb, int first, int tail, int q);
+hipError_t launch_dx_thin_bf16(const LayerArgs& a, hipStream_t s, int ldb, int ra, int first, int tail, int q,
+                               bool clear);
 hipError_t launch_g_bf16(const LayerArgs& a, hipStream_t s);
 hipError_t launch_ste_bf16(const LayerArgs& a, hipStream_t s);  // dB, dA of the straight-through backward
 size_t ste_workspace_bytes(int64_t R, int64_t L, int64_t r);

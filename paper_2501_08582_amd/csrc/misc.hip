@@ -309,9 +309,9 @@ hipError_t launch_split_reduce_bf16(const float* part, int n_full, int split, in
     return hipGetLastError();
 }
 
-TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes) {
-    // compute units of the current device, read once per device (calls from
-    // several host threads may both read it; they store the same value)
+// compute units of the current device, read once per device (calls from
+// several host threads may both read it; they store the same value)
+static int device_cus() {
     static std::atomic<int> cus_of[64];
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
@@ -320,6 +320,11 @@ TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes) {
             cus_of[dev].store(n, std::memory_order_relaxed);
         if (n > 0) cus = n;
     }
+    return cus;
+}
+
+TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes) {
+    const int cus = device_cus();
     TailSplit t{(int)tiles, 1, (int)tiles};
     const int64_t tail = tiles % cus;
     if (tail == 0 || 2 * tail > cus) return t;
@@ -334,6 +339,19 @@ TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes) {
     t.n_full = (int)(tiles - tail);
     t.split = (int)s;
     t.grid = (int)(t.n_full + tail * s);
+    return t;
+}
+
+ThinPlan thin_plan(int64_t tiles) {
+    const int cus = device_cus();
+    ThinPlan t{(int)tiles, 0, 1};
+    const int64_t tail = tiles % cus;
+    if (tail == 0 || 2 * tail > cus) return t;
+    int q = 2;
+    while (q < 8 && 2 * q * tail <= cus) q *= 2;
+    t.n_full = (int)(tiles - tail);
+    t.tail = (int)tail;
+    t.q = q;
     return t;
 }
 

@@ -1,6 +1,8 @@
-"""The library's rule for splitting a short last wave of output tiles over K
-(as documented in include/lors.h), restated for the tests: which shapes split,
-into how many pieces, and which output tiles run in pieces."""
+"""The library's rules for a short last wave of output tiles (as documented in
+include/lors.h), restated for the tests: on whole-tile shapes its tiles are
+cut over their tokens into thin tiles; on other shapes, with
+LORS_FLAG_SPLIT_LAST_WAVE, they are split over K -- which shapes split, into
+how many pieces, and which output tiles run in pieces."""
 
 
 def up256(n):
@@ -45,3 +47,28 @@ def split_tiles(rows, cols, cus=256, group_m=4):
         within = t - g * per_group
         out.append((256 * (first + within % gsz), 256 * (within // gsz)))
     return out
+
+
+def fwd_whole_tiles(L, R, C):
+    """The forward's fixed-offset copies: whole 256 x 256 tiles over L x R,
+    64-wide K-steps over C, 256 slab rows of C bf16 addressed in 32 bits."""
+    return L % 256 == 0 and R % 256 == 0 and C % 64 == 0 and 256 * C * 2 < 2**31
+
+
+def dx_whole_tiles(L, R, C):
+    """The same for dX: tiles over L x C, K-steps over R."""
+    wprT = -(-R // 32)
+    return (L % 256 == 0 and C % 256 == 0 and R % 64 == 0 and 256 * R * 2 < 2**31 and 64 * C * 2 < 2**31
+            and 256 * wprT * 4 < 2**31)
+
+
+def thin_q(tiles, cus=256):
+    """Thin tiles per tile of the short last wave (1: not cut): the largest
+    of 2, 4, 8 whose thin tiles fit on the CUs."""
+    tail = tiles % cus
+    if tail == 0 or 2 * tail > cus:
+        return 1
+    q = 2
+    while q < 8 and 2 * q * tail <= cus:
+        q *= 2
+    return q

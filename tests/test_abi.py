@@ -294,6 +294,8 @@ def test_no_weak_symbol_defined_twice():
     pbuild._check_no_shared_weak_symbols(objs)
 
 
+from split_rule import dx_whole_tiles as _dx_whole  # noqa: E402
+from split_rule import fwd_whole_tiles as _fwd_whole  # noqa: E402
 from split_rule import split_budget as _split_budget  # noqa: E402
 from split_rule import split_bytes as _tail_split_bytes  # noqa: E402
 
@@ -303,27 +305,37 @@ def test_workspace_query_split_last_wave(lib):
     for R, C, L, r in [(5120, 5120, 4096, 64), (4096, 1024, 4352, 16), (4104, 1000, 4300, 5), (4096, 4096, 4096, 16),
                        (256, 256, 256, 8), (4096, 1024, 4352, 100), (13824, 5120, 4096, 64), (16384, 16384, 4352, 16),
                        (65536, 8192, 4352, 64), (8192, 65536, 4352, 16), (32768, 16384, 4352, 16),
+                       (8192, 65536, 4300, 16), (32768, 16384, 4300, 16), (5120, 5120, 4000, 64),
                        # the GPU split tests' shapes
-                       (65792, 1024, 300, 16), (1024, 65792, 256, 64), (1024, 65792, 200, 5),
+                       (65792, 1024, 300, 16), (1024, 65792, 250, 64), (1024, 65792, 200, 5),
                        (1024, 65792, 256, 100)]:
         base = _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r))
         tl = -(-L // 256)
         budget = _split_budget(R, C, r)
-        fwd = _tail_split_bytes(tl * -(-R // 256), -(-C // 64), budget) if r <= 64 else 0
-        dx = _tail_split_bytes(tl * -(-C // 256), -(-R // 64), budget) if -(-r // 8) * 8 <= 64 else 0
+        fwd = dx = 0
+        if r <= 64 and not _fwd_whole(L, R, C):
+            fwd = _tail_split_bytes(tl * -(-R // 256), -(-C // 64), budget)
+        if -(-r // 8) * 8 <= 64 and not _dx_whole(L, R, C):
+            dx = _tail_split_bytes(tl * -(-C // 256), -(-R // 64), budget)
         assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=r, flags=F)) == base + max(fwd, dx), (R, C, L, r)
-    # 5120 x 5120 at 4096 tokens: 320 tiles, a short wave of 64; two pieces of
-    # each would need 32 MiB against a budget of about 3 MiB, so no split
-    assert _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64, flags=F)) == \
-        _lib.workspace_bytes(_p(R=5120, C=5120, L=4096, r=64))
-    # 8192 x 65536 at 4352 tokens: 17 x 32 = 544 forward tiles, a short wave
+    # whole-tile shapes cut their short waves into thin tiles, never over K:
+    # no partials (5120 x 5120 at 4096 tokens: 320 tiles, a short wave of 64)
+    for R, C, L in ((5120, 5120, 4096), (8192, 65536, 4352), (32768, 16384, 4352)):
+        assert _fwd_whole(L, R, C) and _dx_whole(L, R, C)
+        assert _lib.workspace_bytes(_p(R=R, C=C, L=L, r=16, flags=F)) == _lib.workspace_bytes(_p(R=R, C=C, L=L, r=16))
+    # 5120 x 5120 at 4000 tokens (no whole tiles): two pieces of each of the
+    # 64 short-wave tiles would need 32 MiB against a budget of about 3 MiB
+    assert _lib.workspace_bytes(_p(R=5120, C=5120, L=4000, r=64, flags=F)) == \
+        _lib.workspace_bytes(_p(R=5120, C=5120, L=4000, r=64))
+    # 8192 x 65536 at 4300 tokens: 17 x 32 = 544 forward tiles, a short wave
     # of 32; the budget (64 MiB less 256 bytes) holds 7 pieces of each: 56 MiB
-    assert _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16, flags=F)) - \
-        _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16)) == 56 << 20
-    # 32768 x 16384: the dX grid (17 x 64 tiles, a short wave of 64) is cut
-    # into 3 pieces per tile (48 MiB), not the 4 that would fill the CUs
-    assert _lib.workspace_bytes(_p(R=32768, C=16384, L=4352, r=16, flags=F)) - \
-        _lib.workspace_bytes(_p(R=32768, C=16384, L=4352, r=16)) == 48 << 20
+    assert _lib.workspace_bytes(_p(R=8192, C=65536, L=4300, r=16, flags=F)) - \
+        _lib.workspace_bytes(_p(R=8192, C=65536, L=4300, r=16)) == 56 << 20
+    # 32768 x 16384 at 4300 tokens: the dX grid (17 x 64 tiles, a short wave
+    # of 64) is cut into 3 pieces per tile (48 MiB), not the 4 that would fill
+    # the CUs
+    assert _lib.workspace_bytes(_p(R=32768, C=16384, L=4300, r=16, flags=F)) - \
+        _lib.workspace_bytes(_p(R=32768, C=16384, L=4300, r=16)) == 48 << 20
     # no effect for fp32, and none without tokens
     assert _lib.workspace_bytes(_p(dtype=_lib.DTYPE_F32, flags=F)) == 0
     assert _lib.workspace_bytes(_p(L=0, flags=F)) == _lib.workspace_bytes(_p(L=0))
@@ -379,10 +391,10 @@ def test_extents_whose_byte_counts_overflow_are_rejected(lib, R, C, L):
 
 def test_forward_requires_workspace_with_split_flag(lib):
     # validation happens before any HIP call, so this runs without a GPU
-    # 8192 x 65536 at 4352 tokens splits its forward's short wave (see above)
-    p = _p(R=8192, C=65536, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
+    # 8192 x 65536 at 4300 tokens splits its forward's short wave (see above)
+    p = _p(R=8192, C=65536, L=4300, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)
     need = _lib.workspace_bytes(p)
-    assert need > _lib.workspace_bytes(_p(R=8192, C=65536, L=4352, r=16))
+    assert need > _lib.workspace_bytes(_p(R=8192, C=65536, L=4300, r=16))
     # a shape whose budget holds no pieces runs as without the flag, and the
     # forward then needs no workspace: rejected only for its null pointers
     q = _p(R=4096, C=1024, L=4352, r=16, flags=_lib.FLAG_SPLIT_LAST_WAVE)

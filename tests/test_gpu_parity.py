@@ -561,14 +561,15 @@ def test_weight_gradient_tail_split(R, C, L, r, mask):
 # ---------------------------------------------------------------------------
 # LORS_FLAG_SPLIT_LAST_WAVE: forward and dX tiles of a short last wave cut
 # over K, fp32 partials reduced in a fixed order, within a workspace budget
-# of R*C/4 bytes.  Shapes whose grids end in a short wave that the budget can
-# split (tests/split_rule.py restates the rule; test_abi checks the library
-# against it):
+# of R*C/4 bytes -- on shapes without whole tiles (whole-tile shapes cut such
+# waves into thin tiles instead, see test_gpu_thin.py).  Shapes whose grids
+# end in a short wave that the budget can split (tests/split_rule.py restates
+# the rule; test_abi checks the library against it):
 #   65792 x 1024, 300 tokens: forward 2 x 257 tiles (2 in 4 pieces), dX 2 x 4
 #     tiles (all 8 in 4 pieces);
-#   1024 x 65792, 256 tokens: forward 4 tiles in 8 pieces, dX 257 tiles (1 in
-#     4 pieces); rank 5 adds the padded copy of B; rank 100 runs two passes
-#     and is not split.
+#   1024 x 65792, 250 or 200 tokens: forward 4 tiles in 8 pieces, dX 257
+#     tiles (1 in 4 pieces); rank 5 adds the padded copy of B; at 256 tokens
+#     (whole tiles) rank 100 runs two passes and is not split.
 # Split tiles must agree with the unsplit call within one bf16 ulp (the two
 # differ only in fp32 summation order), every other tile bit for bit, and
 # both with the oracle; W is unpruned so that the split pieces also see data
@@ -585,7 +586,7 @@ def _ulp_close(a, b):
 
 
 @pytest.mark.parametrize("R,C,L,r,mask,bias", [(65792, 1024, 300, 16, "magnitude", True),
-                                               (1024, 65792, 256, 64, "2:4", False),
+                                               (1024, 65792, 250, 64, "2:4", False),
                                                (1024, 65792, 200, 5, "magnitude", False),
                                                (1024, 65792, 256, 100, "magnitude", False)])
 def test_split_last_wave(R, C, L, r, mask, bias):
@@ -620,7 +621,8 @@ def test_split_last_wave(R, C, L, r, mask, bias):
     checked = 0
     for name, got, ref0, N, K, ok in (("Y", Y, Y0, R, C, r <= 64), ("dX", dX, dX0, C, R, -(-r // 8) * 8 <= 64)):
         g, u = dev_to_f64(got), dev_to_f64(ref0)
-        split = ok and split_rule.pieces(tl * -(-N // 256), -(-K // 64), budget, cus) > 1
+        whole = (split_rule.fwd_whole_tiles(L, R, C) if name == "Y" else split_rule.dx_whole_tiles(L, R, C))
+        split = ok and not whole and split_rule.pieces(tl * -(-N // 256), -(-K // 64), budget, cus) > 1
         rects = split_rule.split_tiles(L, N, cus) if split else []
         inside = np.zeros(g.shape, dtype=bool)
         for m0, n0 in rects:
