@@ -63,8 +63,8 @@ struct Layout {
     static constexpr int BB = BK * PITCH;          // B slab: 2 KiB per 16 ranks
     static constexpr int D = 0, W = DB, B = DB + WB, M = DB + WB + BB;
     static constexpr int STAGE = DB + WB + BB + MB;
-    static constexpr int LUT = 2 * STAGE;
-    static constexpr int SINK = LUT + 4096;        // 1 KiB target of padding copies
+    static constexpr int LUT = 2 * STAGE;          // select table: 16 x 8 B
+    static constexpr int SINK = LUT + 256;         // 1 KiB target of padding copies
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NBC = BB / 1024;          // 1 KiB copies per B slab
     static constexpr int NB = (NBC + 3) / 4;       // B-slab copies per wave
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     }
 
     // M^T is a plain bitmap whatever the caller's layout.
-    *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<false>((uint32_t)tid);
+    if (tid < 16) *(u32x2*)(smem + Lay::LUT + 8 * tid) = select_lut16_entry<false>((uint32_t)tid);
 
 
     // ---- slab copies.  Copies 0..ND-1: dY slab rows 8*(ND*wave + q) + lane/8
@@ -303,8 +303,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             raw[nb][1] = lo[1];
             raw[nb][2] = hi[0];
             raw[nb][3] = hi[1];
-            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
-            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+            sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
     auto read_d2 = [&](bf16x8 (&df)[MBW], const uint8_t* sb, int c4, int p) {
@@ -331,8 +330,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     auto read_sel = [&](int c4) {
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
-            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
-            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+            sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
     auto unpack = [&](const u32x4 (&rw)[2], int cp, int p) {

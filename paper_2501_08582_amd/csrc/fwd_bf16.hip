@@ -13,8 +13,9 @@
 // 16 accumulator values a lane holds are, in register order, the k values
 // 16c + 8h + {0..7} for c = 0, 1 -- exactly two 32x32x16 B-operand fragments.
 // Each lane then adds its W values (one 16-byte LDS read per fragment), picks
-// the select masks for its eight k from a 256-entry LUT indexed by the mask
-// byte, rounds once to bf16, and feeds the MFMA directly.
+// the select masks for its eight k from a 16-entry table indexed by the two
+// nibbles of the mask byte (128 bytes on distinct LDS banks, so the reads of
+// a wave never conflict), rounds once to bf16, and feeds the MFMA directly.
 //
 // Schedule.  A K-step (64 k) is four sub-steps of 16 k.  While the 16 MFMAs
 // of sub-step c run, the wave reads the X fragments of sub-step c+1 and
@@ -24,9 +25,10 @@
 // formed during sub-step 0.  One barrier per K-step, before sub-step 3:
 // after it the next stage is visible and the current one is free, so
 // sub-step 3 interleaves the first twelve copies of stage kt+2 and the first
-// sub-step of stage kt+1 with its MFMAs; the remaining copies of that stage
-// go out in the merge slots of the next K-step's sub-step 0, still a K-step
-// ahead of the barrier that waits for them.  A wave stalls on a burst of
+// sub-step of stage kt+1 with its MFMAs (those copies have more than a
+// K-step to land); the remaining copies of stage kt+2 go out in the merge
+// slots of the first sub-step of the next K-step, three sub-steps ahead of
+// the barrier that waits for them.  A wave stalls on a burst of
 // asynchronous copies, so spreading them keeps the matrix pipe fed.  X, W, A
 // and mask slabs travel HBM -> LDS with global_load_lds; accumulators
 // (256 x 64 per wave) live in AGPRs.
@@ -65,8 +67,8 @@ struct Layout {
     static constexpr int AB = 16 * RK * kRow64;   // A slab: 16*RK rows of 64 k
     static constexpr int X = 0, W = XB, A = XB + WB, M = XB + WB + AB;
     static constexpr int STAGE = XB + WB + AB + MB;
-    static constexpr int LUT = 2 * STAGE;         // 256 x 16 B
-    static constexpr int SINK = LUT + 4096;       // 1 KiB target of padding copies
+    static constexpr int LUT = 2 * STAGE;         // select table: 16 x 8 B
+    static constexpr int SINK = LUT + 256;        // 1 KiB target of padding copies
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NX = TM / 32;            // X-slab copies per wave
     static constexpr int NAW = (2 * RK + 3) / 4;  // A-slab copies per wave
@@ -133,10 +135,10 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
     const uint8_t* zsrc = (const uint8_t*)g_zero_page + 16 * (lane & 7);
 
-    // ---- select LUT (visible to all waves after the first stage barrier)
+    // ---- select table (visible to all waves after the first stage barrier)
     // and the resident B operand of the merge: column n = 64 wave + 32 nb + l32,
     // ranks 16c + 8h .. +7
-    *(u32x4*)(smem + Lay::LUT + 16 * tid) = select_lut_entry<TWO_FOUR>((uint32_t)tid);
+    if (tid < 16) *(u32x2*)(smem + Lay::LUT + 8 * tid) = select_lut16_entry<TWO_FOUR>((uint32_t)tid);
     const bool b_vec = (r & 7) == 0 && (ldb & 7) == 0;
     bf16x8 bfr[2][RK];
 #pragma unroll
@@ -304,8 +306,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
             raw[nb] = *(const u32x4*)(sb + woff(nb, c4));
-            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
-            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+            sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
     auto read_x2 = [&](bf16x8 (&xf)[MBW], const uint8_t* sb, int c4, int p) {
@@ -325,8 +326,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     auto read_sel = [&](int c4) {
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
-            const uint32_t byte = (mw[nb][c4 >> 1] >> (8 * (2 * (c4 & 1) + h))) & 0xFFu;
-            sel[nb] = *(const u32x4*)(smem + Lay::LUT + 16 * byte);
+            sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
     // pair p of rw, as fp32, into the accumulator half cp of the rank-r block

@@ -95,6 +95,34 @@ __device__ __forceinline__ u32x4 select_lut_entry(uint32_t b) {
     return e;
 }
 
+// Half of a select entry: the two words for four consecutive elements whose
+// keep bits are the nibble n (for the 2:4 layout: whose group code is n).
+// The sixteen half entries make a 128-byte table; it spans distinct LDS
+// banks, so lanes reading it with arbitrary nibbles never conflict (a lane
+// group reading the 256-entry table of whole entries does, about 3.6-way on
+// random masks).
+template <bool TWO_FOUR>
+__device__ __forceinline__ u32x2 select_lut16_entry(uint32_t n) {
+    uint32_t keep = n;
+    if constexpr (TWO_FOUR) keep = (1u << (n & 3u)) | (1u << (n >> 2));
+    u32x2 e;
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+        e[p] = (((keep >> (2 * p)) & 1u) ? 0x0000FFFFu : 0u) | (((keep >> (2 * p + 1)) & 1u) ? 0xFFFF0000u : 0u);
+    return e;
+}
+
+// Select masks of the eight elements whose mask byte starts at bit `shift`
+// of word w, from the 16-entry table at lut (two 8-byte reads).
+__device__ __forceinline__ u32x4 read_sel16(const uint8_t* lut, uint32_t w, uint32_t shift) {
+    // bit-field extracts, so that each address is one more shift-and-add
+    const uint32_t nlo = __builtin_amdgcn_ubfe(w, shift, 4u);
+    const uint32_t nhi = __builtin_amdgcn_ubfe(w, shift + 4u, 4u);
+    const u32x2 lo = *(const u32x2*)(lut + (nlo << 3));
+    const u32x2 hi = *(const u32x2*)(lut + (nhi << 3));
+    return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
 // W' = select(M, W + s.T, 0) for eight consecutive elements: raw holds the
 // eight bf16 of W (pairs), t the eight fp32 rank-r sums, sel the LUT masks.
 __device__ __forceinline__ u32x4 merge8(u32x4 raw, const float* t, float s, u32x4 sel) {
