@@ -317,6 +317,27 @@ def test_no_merged_weight_allocation():
     assert torch.cuda.max_memory_allocated() - base == 0
 
 
+@pytest.mark.parametrize("R,C,L,r", [(1024, 65792, 200, 5),     # forward and dX split over K, partials
+                                     (5120, 5120, 4096, 64)])    # 13B q/k/v/o: thin tiles, no partials
+def test_layer_step_allocates_nothing_and_its_scratch_stays_small(R, C, L, r):
+    """The step the benchmark times (LayerStep: every call with
+    LORS_FLAG_SPLIT_LAST_WAVE): its workspace stays below R*C/4 bytes, an
+    eighth of the bf16 merged weight, and a forward + backward allocates no
+    device memory at all."""
+    from paper_2501_08582_amd.step import LayerStep
+    wl = synth.workload("llama2_7b_q_proj").with_(R=R, C=C, r=r, seed=2200 + r)
+    layer = LayerStep(synth.make(wl, L=L))
+    print("layer step", (R, C, L, r), "workspace", layer.ws, flush=True)
+    assert layer.ws < R * C // 4
+    layer.run()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    layer.run()
+    torch.cuda.synchronize()
+    assert torch.cuda.max_memory_allocated() - base == 0
+
+
 @pytest.mark.parametrize("kind", ["magnitude", "2:4"])
 def test_split_backward_with_mask_reuse(kind):
     """lors_backward_data + lors_backward_weight (reusing the transposed mask
