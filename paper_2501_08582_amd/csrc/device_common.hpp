@@ -121,10 +121,10 @@ __device__ __forceinline__ void work_coords(int bid, int tiles_m, int tiles_n, i
 
 // Tile and sub-tile of a workgroup of a thin-tile grid (see thin_plan in
 // kernels.hpp): logical tiles first .. first+tail-1, in group_coords' order,
-// each cut over its tokens into q sub-tiles u = 0 .. q-1, one per id.  When
-// tail is a multiple of 8, the q sub-tiles of a tile get ids of one XCD (ids
-// are dealt to the 8 XCDs round-robin), so they share its weight slabs in
-// that XCD's L2.
+// each cut into q sub-tiles u = 0 .. q-1, one per id (the kernel maps u to a
+// feature half and a token part).  When tail is a multiple of 8, the q
+// sub-tiles of a tile get ids of one XCD (ids are dealt to the 8 XCDs
+// round-robin), so they share its weight slabs in that XCD's L2.
 __device__ __forceinline__ void thin_coords(int bid, int tiles_m, int tiles_n, int group_m, int first, int tail,
                                             int q, int& tm, int& tn, int& u) {
     int i;

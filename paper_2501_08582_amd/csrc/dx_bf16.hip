@@ -38,14 +38,10 @@ namespace {
 
 constexpr int NT = 256;
 constexpr int BM = 256;  // tokens per tile
-constexpr int BN = 256;  // input features per tile (64 per wave)
+constexpr int BN = 256;  // input features per whole tile (64 per wave)
 constexpr int BK = 64;   // output features (rows of W) per K-step
 constexpr int GROUP_M = 4;
 constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
-
-constexpr int WB = BK * kRowBytes;   // W slab: 4 per-wave blocks of [64 k][64 n], 32 KiB
-constexpr int WBW = WB / 4;          // one wave's block
-constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 
 // B slab [k][rank]: 64 rows of PITCH = 32*RKP bytes (ranks padded to 16*RKP;
 // RKP = RK, except 4 for RK = 3 so that a row holds a power of two of 16-byte
@@ -54,9 +50,20 @@ constexpr int MB = BN * 2 * 4;       // M^T words [n][kb]: 2 KiB
 // apart those rows would fall on only 8 / RKP of the 16 bank groups; the XOR
 // spreads them over all 16 (a 256-byte bank window holds 8 / RKP rows, and
 // bswz takes 2*RKP distinct values over 16 consecutive rows).
-// TM: tokens per tile, BM or (thin tiles of a short last wave) 128, 64, 32
-template <int RK, int TM>
+// TM: tokens per tile, NF: 32-column blocks per wave -- BM and 2 for a whole
+// tile; a thin tile of a short last wave has half the columns (NF = 1) and
+// TM = 256, 128 or 64 tokens.
+// W slab: 4 per-wave blocks of [64 k][32 NF n]; with NF = 2 a block has
+// 128-byte rows in the tr64 layout, with NF = 1 64-byte rows unswizzled (the
+// four rows a 32-lane transpose read covers are then 256 consecutive bytes,
+// one per bank).
+template <int RK, int TM, int NF>
 struct Layout {
+    static constexpr int FT = 128 * NF;            // input features per tile
+    static constexpr int WROW = 64 * NF;           // bytes per row of a wave's W block
+    static constexpr int WBW = BK * WROW;          // one wave's W block
+    static constexpr int WB = 4 * WBW;             // W slab
+    static constexpr int MB = FT * 2 * 4;          // M^T words [n][kb]
     static constexpr int DB = TM * kRow64;         // dY slab: TM rows of 64 k
     static constexpr int RKP = RK == 3 ? 4 : RK;
     static constexpr int PITCH = 32 * RKP;
@@ -69,9 +76,11 @@ struct Layout {
     static constexpr int NBC = BB / 1024;          // 1 KiB copies per B slab
     static constexpr int NB = (NBC + 3) / 4;       // B-slab copies per wave
     static constexpr int ND = TM / 32;             // dY-slab copies per wave
-    static constexpr int COPIES = ND + 8 + NB + 2; // copies per wave per stage
-    static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
-    static_assert(COPIES >= kEarly, "every early copy slot has a copy");
+    static constexpr int NWC = WBW / 1024;         // W-block copies per wave
+    static constexpr int NMC = NF;                 // M^T copies per wave
+    static constexpr int COPIES = ND + NWC + NB + NMC;  // copies per wave per stage
+    static constexpr int EARLY = COPIES < kEarly ? COPIES : kEarly;
+    static_assert(COPIES - EARLY <= 8, "the late copies fit the eight merge slots");
     // physical chunk of logical chunk q in B-slab row k
     static __device__ __forceinline__ int bswz(int k, int q) { return q ^ ((k / (8 / RKP)) & (2 * RKP - 1)); }
 };
@@ -85,24 +94,24 @@ struct Layout {
 // taken as zero and the product is added onto dX.  ldb: row stride of B.
 // r: the rank the kernel works on, a multiple of 8 (B's columns ra .. r-1
 // are zero); ra: the rows of A that exist (A rows ra .. r-1 are read as zero).
-// TM < BM: a thin tile of TM tokens and BN features (whole-tile shapes only),
-// as in the forward kernel.
-template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM>
+// TM, NF < (BM, 2): a thin tile of TM tokens and 128 NF input features
+// (whole-tile shapes, one pass), as in the forward kernel.
+template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM, int NF>
 __global__ __launch_bounds__(NT, 1) void dx_kernel(
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mt, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, uint16_t* __restrict__ dX, int64_t L, int R, int C, int r,
     int ra, float s, int tiles_m, int tiles_n, int ldb, float* __restrict__ z0, int64_t nz0,
     float* __restrict__ z1, int64_t nz1, int n_full, int split, float* __restrict__ part) {
-    using Lay = Layout<RK, TM>;
+    using Lay = Layout<RK, TM, NF>;
     constexpr int MBW = TM / 32;  // 32-token blocks per wave
-    static_assert(TM == BM || (!RAGGED && !PASS2), "thin tiles: fixed-offset copies, one pass");
+    static_assert((TM == BM && NF == 2) || (!RAGGED && !PASS2), "thin tiles: fixed-offset copies, one pass");
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
-    static_assert(4 * TM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
+    static_assert(4 * TM * 64 * NF <= 2 * Lay::STAGE, "output staging fits the stage buffers");
     // the prologue parks the merge's A block in stage 1: in its dY region,
     // clear of the W slabs that PASS2 zeroes once (a thin tile's dY region is
     // smaller, but it has no second pass and may use the whole stage)
-    static_assert(16 * RK * kRowBytes <= (TM == BM ? Lay::DB : Lay::STAGE), "A block fits stage 1");
+    static_assert(16 * RK * kRowBytes <= (PASS2 ? Lay::DB : Lay::STAGE), "A block fits stage 1");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -125,21 +134,24 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     // tile and K-steps: ids past n_full are pieces of split tiles (their
     // partial sums go to `part`, see the epilogue).  Thin tiles: the grid
     // covers logical tiles n_full .. n_full+split-1, each cut into BM/TM
-    // (see thin_coords), with every K-step.
+    // token parts of each of its 2/NF feature parts (see thin_coords), with
+    // every K-step.
     int tm, tn;
     int kbeg, nk;
     int64_t m0;
-    if constexpr (TM == BM) {
+    int n0;
+    if constexpr (TM == BM && NF == 2) {
         work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (R + BK - 1) / BK, tm, tn, kbeg, nk);
         m0 = (int64_t)tm * BM;
+        n0 = tn * BN;
     } else {
         int u;
-        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, BM / TM, tm, tn, u);
+        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (BM / TM) * (2 / NF), tm, tn, u);
         kbeg = 0;
         nk = (R + BK - 1) / BK;
-        m0 = (int64_t)tm * BM + (int64_t)u * TM;
+        m0 = (int64_t)tm * BM + (int64_t)(u % (BM / TM)) * TM;
+        n0 = tn * BN + (u / (BM / TM)) * Lay::FT;
     }
-    const int n0 = tn * BN;
     const int kofs = kbeg * BK;
     const int wprT = (R + 31) >> 5;  // words per row of M^T
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
@@ -165,23 +177,30 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
 
 
     // ---- slab copies.  Copies 0..ND-1: dY slab rows 8*(ND*wave + q) + lane/8
-    // (64 k per row); copies ND..ND+7: rows 8q + lane/8 (k) of this wave's W
-    // block, its 64 columns; then the B slab and the M^T words.
-    uint32_t offD[Lay::ND], offW[8];
+    // (64 k per row); copies ND..ND+NWC-1: this wave's W block, its 32 NF
+    // columns (NF = 2: rows 8q + lane/8 in the tr64 layout; NF = 1: rows
+    // 16q + lane/4, 16-byte chunk lane % 4); then the B slab and the M^T
+    // words.
+    uint32_t offD[Lay::ND], offW[Lay::NWC];
 #pragma unroll
     for (int q = 0; q < Lay::ND; ++q) {
         const int rd = 8 * (Lay::ND * wave + q) + (lane >> 3);
         offD[q] = (uint32_t)((rd * R + 8 * ((lane & 7) ^ ((rd >> 1) & 7))) * 2);
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int rw = 8 * q + (lane >> 3);
-        offW[q] = (uint32_t)((rw * C + 64 * wave + 8 * ((lane & 7) ^ tr64_swz(rw))) * 2);
+    for (int q = 0; q < Lay::NWC; ++q) {
+        if constexpr (NF == 2) {
+            const int rw = 8 * q + (lane >> 3);
+            offW[q] = (uint32_t)((rw * C + 64 * wave + 8 * ((lane & 7) ^ tr64_swz(rw))) * 2);
+        } else {
+            const int rw = 16 * q + (lane >> 2);
+            offW[q] = (uint32_t)((rw * C + 32 * wave + 8 * (lane & 3)) * 2);
+        }
     }
-    uint32_t offM[2];
+    uint32_t offM[Lay::NMC];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int e = 64 * (2 * wave + q) + lane;
+    for (int q = 0; q < Lay::NMC; ++q) {
+        const int e = 64 * (Lay::NMC * wave + q) + lane;
         offM[q] = (uint32_t)(((e >> 1) * wprT + (e & 1)) * 4);
     }
     const uint16_t* Dt = uniform_ptr(dY + m0 * R);
@@ -201,10 +220,10 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 const bool ok = m0 + row < L && k0 + 8 * lc < R;
                 copy16_to_lds(ok ? (const void*)(Dt + (int64_t)row * R + k0 + 8 * lc) : (const void*)zsrc, dst);
             }
-        } else if (j < Lay::ND + 8) {
+        } else if (j < Lay::ND + Lay::NWC) {
             if (PASS2) return;  // W is zero: its slabs were cleared once
             const int q = j - Lay::ND;
-            const uint32_t dst = sb + Lay::W + WBW * wave + 1024 * q;
+            const uint32_t dst = sb + Lay::W + Lay::WBW * wave + 1024 * q;
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr(Wn + (int64_t)k0 * C), offW[q], dst);
             } else {
@@ -213,21 +232,21 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                 const bool ok = k0 + row < R && n0 + col < C;
                 copy16_to_lds(ok ? (const void*)(Wn + (int64_t)(k0 + row) * C + col) : (const void*)zsrc, dst);
             }
-        } else if (j < Lay::ND + 8 + Lay::NB) {
+        } else if (j < Lay::ND + Lay::NWC + Lay::NB) {
             // the swizzled B slab of rows k0 .. k0+63; every wave issues NB
             // copies, those past the slab go to the sink
-            const int q = j - Lay::ND - 8, blk = 4 * q + wave;
+            const int q = j - Lay::ND - Lay::NWC, blk = 4 * q + wave;
             const bool real = blk < Lay::NBC;
             const bool ok = bval[q] && (!RAGGED || k0 + brow[q] < R);
             const void* src = (const uint8_t*)Bm + ((int64_t)k0 + brow[q]) * (2 * (int64_t)ldb) + bcol[q];
             copy16_to_lds(ok ? src : (const void*)zsrc, real ? sb + Lay::B + 1024 * blk : lds0 + Lay::SINK);
         } else {
-            const int q = j - Lay::ND - 8 - Lay::NB;
-            const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
+            const int q = j - Lay::ND - Lay::NWC - Lay::NB;
+            const uint32_t dst = sb + Lay::M + 256 * (Lay::NMC * wave + q);
             if constexpr (!RAGGED) {
                 copy4s_to_lds(uniform_ptr(Mn + (k0 >> 5)), offM[q], dst);
             } else {
-                const int e = 64 * (2 * wave + q) + lane;
+                const int e = 64 * (Lay::NMC * wave + q) + lane;
                 const int n = e >> 1, gw = (k0 >> 5) + (e & 1);
                 const bool ok = n0 + n < C && gw < wprT;
                 copy4_to_lds(ok ? (const void*)(Mn + (int64_t)n * wprT + gw) : (const void*)zsrc, dst);
@@ -238,44 +257,45 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     // Rows of the merge A operand: lane (rho = l32, h) reads B row pi(rho).
     const int rho = l32;
     const int pik = 16 * (rho >> 4) + 8 * ((rho >> 2) & 1) + 4 * ((rho >> 3) & 1) + (rho & 3);
-    const int ncol0 = 64 * wave + l32;
+    const int ncol0 = 32 * NF * wave + l32;
     // transpose-read offsets of the raw W fragments in this wave's W block,
     // sub-step 0 (sub-step c4 is 16 rows further): group g of 16 lanes reads
     // rows 8(g/2) + 4t + 0..3, columns 32nb + 16(g%2) + 0..15
-    int offWt[2][2];
+    int offWt[NF][2];
     {
         const int g = lane >> 4, jj = lane & 15;
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
-                offWt[nb][t] = Lay::W + WBW * wave +
-                               tr64_elem_off(8 * (g >> 1) + 4 * t + (jj >> 2), 32 * nb + 16 * (g & 1) + 4 * (jj & 3));
+            for (int t = 0; t < 2; ++t) {
+                const int row = 8 * (g >> 1) + 4 * t + (jj >> 2), col = 32 * nb + 16 * (g & 1) + 4 * (jj & 3);
+                offWt[nb][t] = Lay::W + Lay::WBW * wave + (NF == 2 ? tr64_elem_off(row, col) : row * Lay::WROW + 2 * col);
+            }
     }
     auto doff = [&](int mb, int c4) { return Lay::D + slab64_off(32 * mb + l32, 2 * c4 + h); };
 
-    f32x16 acc[MBW][2];
+    f32x16 acc[MBW][NF];
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NF; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
     bf16x8 da[MBW], db[MBW];  // dY fragments of alternate sub-steps
-    u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
-    f32x16 T[2];              // rank-r block of the current 32-wide k half
-    uint32_t mw[2][2];        // M^T words [nb][kb] of the current K-step
-    u32x4 raw[2], sel[2];
-    u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
+    u32x4 wa[NF], wb[NF];     // W' fragments of alternate sub-steps
+    f32x16 T[NF];             // rank-r block of the current 32-wide k half
+    uint32_t mw[NF][2];       // M^T words [nb][kb] of the current K-step
+    u32x4 raw[NF], sel[NF];
+    u32x4 rwa[NF], rwb[NF];   // folded merge: W of the two sub-steps of a k half
     bf16x8 bfr[RK];           // B[32kb + pi(rho)][16c + 8h .. +7]
-    bf16x8 afr[2][RK];        // A[16c + 8h .. +7][n] (scaled by s when the merge is folded)
+    bf16x8 afr[NF][RK];       // A[16c + 8h .. +7][n] (scaled by s when the merge is folded)
 
     // MFMA slot i of a sub-step: token block i/2, feature block i%2 (the
     // slots of token blocks a thin tile lacks are empty)
-    auto mm = [&](int i, const bf16x8 (&df)[MBW], const u32x4 (&wf)[2]) {
+    auto mm = [&](int i, const bf16x8 (&df)[MBW], const u32x4 (&wf)[NF]) {
         const int mb = i >> 1, nb = i & 1;
-        if (mb < MBW) acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+        if (mb < MBW && nb < NF) acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
     };
     // ranks 16c + 8h .. +7 of B row 32kb + pik; the slab holds zeros for
     // ranks at or past r, so the read needs no per-lane test (a lane-dependent
@@ -288,7 +308,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     };
     auto read_mw = [&](const uint8_t* sb) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NF; ++nb) {
             const u32x2 v = *(const u32x2*)(sb + Lay::M + 8 * (ncol0 + 32 * nb));
             mw[nb][0] = v[0];
             mw[nb][1] = v[1];
@@ -296,9 +316,9 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     };
     auto read_rs = [&](const uint8_t* sb, int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRow64);
-            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRow64);
+        for (int nb = 0; nb < NF; ++nb) {
+            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * Lay::WROW);
+            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * Lay::WROW);
             raw[nb][0] = lo[0];
             raw[nb][1] = lo[1];
             raw[nb][2] = hi[0];
@@ -310,17 +330,18 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         if (2 * p < MBW) df[2 * p] = *(const bf16x8*)(sb + doff(2 * p, c4));
         if (2 * p + 1 < MBW) df[2 * p + 1] = *(const bf16x8*)(sb + doff(2 * p + 1, c4));
     };
-    auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
+    auto merge_piece = [&](u32x4 (&wf)[NF], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
-        wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
+        if (nb < NF)
+            wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
     };
     // folded merge (see the forward kernel): raw W of sub-step c4, its select
     // masks, the unpack of a W pair into the rank-r accumulator, the merge
-    auto read_raw = [&](u32x4 (&rw)[2], const uint8_t* sb, int c4) {
+    auto read_raw = [&](u32x4 (&rw)[NF], const uint8_t* sb, int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * kRow64);
-            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * kRow64);
+        for (int nb = 0; nb < NF; ++nb) {
+            const u32x2 lo = lds_tr_read(sb + offWt[nb][0] + 16 * c4 * Lay::WROW);
+            const u32x2 hi = lds_tr_read(sb + offWt[nb][1] + 16 * c4 * Lay::WROW);
             rw[nb][0] = lo[0];
             rw[nb][1] = lo[1];
             rw[nb][2] = hi[0];
@@ -329,22 +350,24 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     };
     auto read_sel = [&](int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NF; ++nb) {
             sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
-    auto unpack = [&](const u32x4 (&rw)[2], int cp, int p) {
+    auto unpack = [&](const u32x4 (&rw)[NF], int cp, int p) {
         const int nb = p >> 2, q = p & 3;
-        T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
-        T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+        if (nb < NF) {
+            T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
+            T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+        }
     };
-    auto merge_fold = [&](u32x4 (&wf)[2], int p, int cp) {
+    auto merge_fold = [&](u32x4 (&wf)[NF], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
-        wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
+        if (nb < NF) wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
     };
-    // late_*: the copies kEarly.. of the stage in the other buffer, issued in
+    // late_*: the copies EARLY.. of the stage in the other buffer, issued in
     // the merge slots of the first sub-step of a K-step (see the main loop)
-    auto substep = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[2], bf16x8 (&dn)[MBW], u32x4 (&wn)[2],
+    auto substep = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[NF], bf16x8 (&dn)[MBW], u32x4 (&wn)[NF],
                        const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
                        bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
@@ -359,7 +382,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, dc, wc);
             merge_piece(wn, p, c4n & 1);
-            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            if (late_on && Lay::EARLY + p < Lay::COPIES) copy_j(Lay::EARLY + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, dc, wc);
@@ -367,7 +390,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         SLOT_END();
     };
     // the sub-steps with the folded merge (schedule as in the forward)
-    auto substep_fold = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[2], bf16x8 (&dn)[MBW], u32x4 (&wn)[2],
+    auto substep_fold = [&](const bf16x8 (&dc)[MBW], const u32x4 (&wc)[NF], bf16x8 (&dn)[MBW], u32x4 (&wn)[NF],
                             const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
                             uint32_t late_sq = 0, bool late_on = false) {
         const int cp = c4n & 1;
@@ -379,7 +402,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             read_d2(dn, sb, c4n, i);
             if (c4n == 1) { unpack(rwa, 0, 2 * i); unpack(rwa, 0, 2 * i + 1); }
             if (c4n == 3 && i == 3) {
-                wait_vmcnt<Lay::NB + 2>();  // this wave's W copies of the next stage
+                wait_vmcnt<Lay::NB + Lay::NMC>();  // this wave's W copies of the next stage
                 read_raw(rwa, snext, 0);
                 read_raw(rwb, snext, 1);
             }
@@ -392,7 +415,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             merge_fold(wn, p, cp);
             if (c4n == 1) unpack(rwb, 1, p);
             if (c4n == 3) { unpack(rwb, 1, p); unpack(rwa, 0, p); }
-            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            if (late_on && Lay::EARLY + p < Lay::COPIES) copy_j(Lay::EARLY + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, dc, wc);
@@ -401,8 +424,8 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     };
 
     if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
-        for (int i = tid; i < 2 * (WB / 16); i += NT)
-            *(u32x4*)(smem + (i / (WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (WB / 16))) = zero_u32x4();
+        for (int i = tid; i < 2 * (Lay::WB / 16); i += NT)
+            *(u32x4*)(smem + (i / (Lay::WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (Lay::WB / 16))) = zero_u32x4();
         __syncthreads();
     }
 
@@ -425,14 +448,14 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     stage_barrier<0>();
     // the merge's B operand A[16c + 8h + e][n] into registers via transpose loads
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
         for (int c = 0; c < RK; ++c)
-            afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 0)),
-                                      lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 64 * wave + 32 * nb, 1)));
+            afr[nb][c] = frag_from_tr(lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 32 * NF * wave + 32 * nb, 0)),
+                                      lds_tr_read(smem + Lay::STAGE + tr_frag_off(lane, 16 * c, 32 * NF * wave + 32 * nb, 1)));
     if constexpr (FOLD) {  // s.A, exact for a power-of-two s
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
             for (int c = 0; c < RK; ++c) {
                 u32x4 v = __builtin_bit_cast(u32x4, afr[nb][c]);
@@ -474,7 +497,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const int st = kt & 1;
         const uint8_t* sb = smem + st * Lay::STAGE;
         const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
-        // copies kEarly.. of stage kt+1 (buffer st^1, free since the last
+        // copies EARLY.. of stage kt+1 (buffer st^1, free since the last
         // barrier; the barrier below waits for them); at kt = 0 the prologue
         // issued all of stage 1
         const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
@@ -492,41 +515,44 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
         const uint32_t sq = lds0 + st * Lay::STAGE;
         // one copy per MFMA slot: a copy issued behind an MFMA stalls the
         // wave while that MFMA runs, a second one would stall the next
-        mm(0, db, wb); read_mw(sn); read_bfr(sn, 0); copy_j(0, k2, sq); SLOT_END();
-        mm(1, db, wb); copy_j(1, k2, sq); SLOT_END();
-        mm(2, db, wb); read_d2(da, sn, 0, 0); copy_j(2, k2, sq); SLOT_END();
-        mm(3, db, wb); read_d2(da, sn, 0, 1); copy_j(3, k2, sq); SLOT_END();
+        auto early = [&](int j) {
+            if (j < Lay::EARLY) copy_j(j, k2, sq);
+        };
+        mm(0, db, wb); read_mw(sn); read_bfr(sn, 0); early(0); SLOT_END();
+        mm(1, db, wb); early(1); SLOT_END();
+        mm(2, db, wb); read_d2(da, sn, 0, 0); early(2); SLOT_END();
+        mm(3, db, wb); read_d2(da, sn, 0, 1); early(3); SLOT_END();
         mm(4, db, wb);
         if constexpr (FOLD) read_sel(0);
         else read_rs(sn, 0);
-        copy_j(4, k2, sq); SLOT_END();
-        mm(5, db, wb); read_d2(da, sn, 0, 2); copy_j(5, k2, sq); SLOT_END();
+        early(4); SLOT_END();
+        mm(5, db, wb); read_d2(da, sn, 0, 2); early(5); SLOT_END();
         mm(6, db, wb); read_d2(da, sn, 0, 3);
         if constexpr (FOLD) rank_mfma2_acc<RK>(T, bfr, afr);
         else rank_mfma2<RK>(T, bfr, afr);
-        copy_j(6, k2, sq); SLOT_END();
+        early(6); SLOT_END();
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, db, wb);
             if constexpr (FOLD) merge_fold(wa, p, 0);
             else merge_piece(wa, p, 0);
-            if (7 + p < kEarly) copy_j(7 + p, k2, sq);
+            early(7 + p);
             SLOT_END();
         }
         mm(15, db, wb);
         SLOT_END();
     }
-    // ---- epilogue: round to bf16, stage the wave's TM x 64 block in LDS
-    // (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
+    // ---- epilogue: round to bf16, stage the wave's TM x 32 NF block in LDS
+    // (rows of 32 NF outputs), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
-    if (TM == BM && (int)blockIdx.x >= n_full) {
+    if (TM == BM && NF == 2 && (int)blockIdx.x >= n_full) {
         // a piece of a split tile: its unrounded fp32 partial sums go to slice
         // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
         // reduction launch adds the pieces in order and rounds once
         float* dst = part + (int64_t)((int)blockIdx.x - n_full) * (BM * BN);
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
             for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
@@ -534,20 +560,22 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
                     dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + ncol0 + 32 * nb] = acc[mb][nb][v];
         return;
     }
-    uint16_t* ol = (uint16_t*)(smem + wave * (TM * 128));
+    constexpr int OW = 32 * NF;   // outputs per staged row
+    constexpr int CH = OW / 8;    // 16-byte chunks per row
+    uint16_t* ol = (uint16_t*)(smem + wave * (TM * OW * 2));
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
         for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
-                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v]);
+                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * OW + 32 * nb + l32] = bf16_bits(acc[mb][nb][v]);
 #pragma unroll 4
-    for (int it = 0; it < TM / 8; ++it) {
-        const int row = 8 * it + (lane >> 3), ch = lane & 7;
-        const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
+    for (int it = 0; it < TM * CH / 64; ++it) {
+        const int row = (64 / CH) * it + lane / CH, ch = lane % CH;
+        const u32x4 v = *(const u32x4*)(ol + row * OW + 8 * ch);
         const int64_t gm = m0 + row;
-        const int gn = n0 + 64 * wave + 8 * ch;
+        const int gn = n0 + OW * wave + 8 * ch;
         if (gm < L && gn < C) {
             if constexpr (PASS2)
                 *(u32x4*)(dX + gm * C + gn) = add_bf16x8(*(const u32x4*)(dX + gm * C + gn), v);
@@ -565,10 +593,10 @@ bool power_of_two(float s) {
 }
 
 // z0, z1: dB (R x rank) and dA (rank x C) to clear, or null
-template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM>
+template <int RK, bool RAGGED, bool PASS2, bool FOLD, int TM, int NF>
 void launch_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, int grid, int tiles_m, int tiles_n, int n_full,
                int split, float* part, float* z0, int64_t nz0, float* z1, int64_t nz1) {
-    hipLaunchKernelGGL((dx_kernel<RK, RAGGED, PASS2, FOLD, TM>), dim3(grid), dim3(NT), 0, st, (const uint16_t*)a.dY,
+    hipLaunchKernelGGL((dx_kernel<RK, RAGGED, PASS2, FOLD, TM, NF>), dim3(grid), dim3(NT), 0, st, (const uint16_t*)a.dY,
                        (const uint16_t*)a.W, a.Mt, (const uint16_t*)a.B, (const uint16_t*)a.A, (uint16_t*)a.dX, a.L,
                        (int)a.R, (int)a.C, (int)a.r, ra, a.scale, tiles_m, tiles_n, ldb, z0, nz0, z1, nz1, n_full,
                        split, part);
@@ -605,13 +633,13 @@ hipError_t launch_rk(const LayerArgs& a, hipStream_t st, int ldb, int ra, bool c
     const int64_t nz0 = clear_here ? a.R * a.r_grad : 0, nz1 = clear_here ? a.r_grad * a.C : 0;
     if (grid > 0) {
         if (ragged)
-            launch_tm<RK, true, PASS2, false, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
+            launch_tm<RK, true, PASS2, false, BM, 2>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
                                                   nz0, z1, nz1);
         else if (fold)
-            launch_tm<RK, false, PASS2, true, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
+            launch_tm<RK, false, PASS2, true, BM, 2>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part, z0,
                                                   nz0, z1, nz1);
         else
-            launch_tm<RK, false, PASS2, false, BM>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part,
+            launch_tm<RK, false, PASS2, false, BM, 2>(a, st, ldb, ra, grid, tiles_m, tiles_n, n_full, sp.split, part,
                                                    z0, nz0, z1, nz1);
     }
     hipError_t e = hipGetLastError();
@@ -638,6 +666,7 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb,
 
 #else  // LORS_THIN_TILES
 
+// thin tiles of one feature half (NF = 1) and TM tokens: 2 BM / TM per tile
 template <int RK, bool FOLD, int TM>
 hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, bool clear) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
@@ -645,7 +674,7 @@ hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, i
     float* z0 = clear ? a.dB : nullptr;
     float* z1 = clear ? a.dA : nullptr;
     const int64_t nz0 = clear ? a.R * a.r_grad : 0, nz1 = clear ? a.r_grad * a.C : 0;
-    launch_tm<RK, false, false, FOLD, TM>(a, st, ldb, ra, tail * (BM / TM), tiles_m, tiles_n, first, tail, nullptr,
+    launch_tm<RK, false, false, FOLD, TM, 1>(a, st, ldb, ra, tail * (2 * BM / TM), tiles_m, tiles_n, first, tail, nullptr,
                                           z0, nz0, z1, nz1);
     return hipGetLastError();
 }
@@ -653,10 +682,10 @@ hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int ra, i
 template <int RK, bool FOLD>
 hipError_t launch_thin_q(const LayerArgs& a, hipStream_t st, int ldb, int ra, int first, int tail, int q,
                          bool clear) {
-    switch (q) {
-        case 2: return launch_thin_tm<RK, FOLD, BM / 2>(a, st, ldb, ra, first, tail, clear);
-        case 4: return launch_thin_tm<RK, FOLD, BM / 4>(a, st, ldb, ra, first, tail, clear);
-        case 8: return launch_thin_tm<RK, FOLD, BM / 8>(a, st, ldb, ra, first, tail, clear);
+    switch (q) {  // q thin tiles per tile: two feature halves, each cut into q/2 token parts
+        case 2: return launch_thin_tm<RK, FOLD, BM>(a, st, ldb, ra, first, tail, clear);
+        case 4: return launch_thin_tm<RK, FOLD, BM / 2>(a, st, ldb, ra, first, tail, clear);
+        case 8: return launch_thin_tm<RK, FOLD, BM / 4>(a, st, ldb, ra, first, tail, clear);
         default: return hipErrorInvalidValue;
     }
 }

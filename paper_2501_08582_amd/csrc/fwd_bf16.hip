@@ -52,18 +52,20 @@ namespace {
 
 constexpr int NT = 256;
 constexpr int BM = 256;   // tokens per tile
-constexpr int BN = 256;   // output features per tile (64 per wave)
+constexpr int BN = 256;   // output features per whole tile (64 per wave)
 constexpr int BK = 64;    // input features per K-step
 constexpr int GROUP_M = 4;
 constexpr int kEarly = 12;  // copies of a stage issued right after the barrier; the rest a sub-step later
 
-constexpr int WB = BN * kRow64;  // 32 KiB
-constexpr int MB = BN * 2 * 4;   // 2 mask words per row of W: 2 KiB
-
-// TM: tokens per tile, BM or (thin tiles of a short last wave) 128, 64, 32
-template <int RK, int TM>
+// TM: tokens per tile, NF: 32-feature blocks per wave -- BM and 2 for a whole
+// tile; a thin tile of a short last wave has half the features (NF = 1) and
+// TM = 256, 128 or 64 tokens
+template <int RK, int TM, int NF>
 struct Layout {
+    static constexpr int FT = 128 * NF;           // output features per tile
     static constexpr int XB = TM * kRow64;        // X slab: TM rows of 64 k
+    static constexpr int WB = FT * kRow64;        // W slab: FT rows of 64 k
+    static constexpr int MB = FT * 2 * 4;         // 2 mask words per row of W
     static constexpr int AB = 16 * RK * kRow64;   // A slab: 16*RK rows of 64 k
     static constexpr int X = 0, W = XB, A = XB + WB, M = XB + WB + AB;
     static constexpr int STAGE = XB + WB + AB + MB;
@@ -71,10 +73,12 @@ struct Layout {
     static constexpr int SINK = LUT + 256;        // 1 KiB target of padding copies
     static constexpr int TOTAL = SINK + 1024;
     static constexpr int NX = TM / 32;            // X-slab copies per wave
+    static constexpr int NWC = 4 * NF;            // W-slab copies per wave
     static constexpr int NAW = (2 * RK + 3) / 4;  // A-slab copies per wave
-    static constexpr int COPIES = NX + 8 + NAW + 2;  // copies per wave per stage
-    static_assert(COPIES - kEarly <= 8, "the late copies fit the eight merge slots");
-    static_assert(COPIES >= kEarly, "every early copy slot has a copy");
+    static constexpr int NMC = NF;                // mask copies per wave
+    static constexpr int COPIES = NX + NWC + NAW + NMC;  // copies per wave per stage
+    static constexpr int EARLY = COPIES < kEarly ? COPIES : kEarly;
+    static_assert(COPIES - EARLY <= 8, "the late copies fit the eight merge slots");
 };
 
 #define SLOT_END() __builtin_amdgcn_sched_barrier(0)
@@ -89,21 +93,23 @@ struct Layout {
 // K-chunk is in range and copies use a uniform base plus fixed offsets.
 // PASS2: the second pass of a rank above 64 (ranks 64.. of B and A): W is
 // taken as zero and the product is added onto Y.  ldb: row stride of B.
-// TM < BM: a thin tile of TM tokens and BN features (whole-tile shapes only);
-// each wave then holds TM x 64 accumulators and the MFMA slots and X reads
-// of the missing token blocks drop out of the schedule.
-template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD, int TM>
+// TM, NF < (BM, 2): a thin tile of TM tokens and 128 NF features
+// (whole-tile shapes, one pass); each wave then holds TM x 32 NF
+// accumulators, merges 32 NF rows of W', and the MFMA slots, X reads and
+// merge pieces of the missing token and feature blocks drop out of the
+// schedule.
+template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD, int TM, int NF>
 __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const uint32_t* __restrict__ Mp, const uint16_t* __restrict__ Bm,
     const uint16_t* __restrict__ Am, const uint16_t* __restrict__ bias,
     uint16_t* __restrict__ Y, int64_t L, int R, int C, int r, float s, int tiles_m,
     int tiles_n, int ldb, int n_full, int split, float* __restrict__ part) {
-    using Lay = Layout<RK, TM>;
+    using Lay = Layout<RK, TM, NF>;
     constexpr int MBW = TM / 32;  // 32-token blocks per wave
-    static_assert(TM == BM || !RAGGED, "thin tiles take the fixed-offset copies");
+    static_assert((TM == BM && NF == 2) || (!RAGGED && !PASS2), "thin tiles: fixed-offset copies, one pass");
     static_assert(Lay::TOTAL <= 160 * 1024, "LDS budget");
-    static_assert(4 * TM * 128 <= 2 * Lay::STAGE, "output staging fits the stage buffers");
+    static_assert(4 * TM * 64 * NF <= 2 * Lay::STAGE, "output staging fits the stage buffers");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Lay::TOTAL];
 
     const int tid = threadIdx.x;
@@ -115,21 +121,24 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // tile and K-steps: ids past n_full are pieces of split tiles (their
     // partial sums go to `part`, see the epilogue).  Thin tiles: the grid
     // covers logical tiles n_full .. n_full+split-1, each cut into BM/TM
-    // (see thin_coords), with every K-step.
+    // token parts of each of its 2/NF feature parts (see thin_coords), with
+    // every K-step.
     int tm, tn;
     int kbeg, nk;
     int64_t m0;
-    if constexpr (TM == BM) {
+    int n0;
+    if constexpr (TM == BM && NF == 2) {
         work_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (C + BK - 1) / BK, tm, tn, kbeg, nk);
         m0 = (int64_t)tm * BM;
+        n0 = tn * BN;
     } else {
         int u;
-        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, BM / TM, tm, tn, u);
+        thin_coords(blockIdx.x, tiles_m, tiles_n, GROUP_M, n_full, split, (BM / TM) * (2 / NF), tm, tn, u);
         kbeg = 0;
         nk = (C + BK - 1) / BK;
-        m0 = (int64_t)tm * BM + (int64_t)u * TM;
+        m0 = (int64_t)tm * BM + (int64_t)(u % (BM / TM)) * TM;
+        n0 = tn * BN + (u / (BM / TM)) * Lay::FT;
     }
-    const int n0 = tn * BN;
     const int kofs = kbeg * BK;
     const int wpr = (C + 31) >> 5;
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
@@ -140,10 +149,10 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // ranks 16c + 8h .. +7
     if (tid < 16) *(u32x2*)(smem + Lay::LUT + 8 * tid) = select_lut16_entry<TWO_FOUR>((uint32_t)tid);
     const bool b_vec = (r & 7) == 0 && (ldb & 7) == 0;
-    bf16x8 bfr[2][RK];
+    bf16x8 bfr[NF][RK];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int gn = n0 + 64 * wave + 32 * nb + l32;
+    for (int nb = 0; nb < NF; ++nb) {
+        const int gn = n0 + 32 * NF * wave + 32 * nb + l32;
 #pragma unroll
         for (int c = 0; c < RK; ++c) {
             u32x4 v = zero_u32x4();
@@ -168,10 +177,10 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     }
 
     // ---- slab copies.  Copy q < NX of a wave fills X slab rows
-    // 8*(NX*wave + q) + lane/8, copy NX + q (q < 8) W slab rows
-    // 8*(8*wave + q) + lane/8; lane l covers physical chunk l % 8 of its row.
-    // (With whole tiles NX = 8 and the two share their offsets.)
-    uint32_t offX[Lay::NX], offW[8];
+    // 8*(NX*wave + q) + lane/8, copy NX + q (q < NWC) W slab rows
+    // 8*(NWC*wave + q) + lane/8; lane l covers physical chunk l % 8 of its
+    // row.  (With whole tiles NX = NWC = 8 and the two share their offsets.)
+    uint32_t offX[Lay::NX], offW[Lay::NWC];
 #pragma unroll
     for (int q = 0; q < Lay::NX; ++q) {
         const int row = 8 * (Lay::NX * wave + q) + (lane >> 3);
@@ -179,8 +188,8 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         offX[q] = (uint32_t)((row * C + 8 * lc) * 2);
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int row = 8 * (8 * wave + q) + (lane >> 3);
+    for (int q = 0; q < Lay::NWC; ++q) {
+        const int row = 8 * (Lay::NWC * wave + q) + (lane >> 3);
         const int lc = (lane & 7) ^ ((row >> 1) & 7);
         offW[q] = (uint32_t)((row * C + 8 * lc) * 2);
     }
@@ -193,11 +202,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const int lc = (lane & 7) ^ tr64_swz(row);
         aptr[q] = Am + (int64_t)row * C + 8 * lc;
     }
-    // mask words [row n][kb]: two 256-byte copies per wave
-    uint32_t offM[2];
+    // mask words [row n][kb]: NMC 256-byte copies per wave
+    uint32_t offM[Lay::NMC];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int e = 64 * (2 * wave + q) + lane;
+    for (int q = 0; q < Lay::NMC; ++q) {
+        const int e = 64 * (Lay::NMC * wave + q) + lane;
         offM[q] = (uint32_t)(((e >> 1) * wpr + (e & 1)) * 4);
     }
     const uint16_t* Xt = uniform_ptr(X + m0 * C);
@@ -207,11 +216,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // copy j of the stage at K offset k0 into the stage at LDS address sb
     auto copy_j = [&](int j, int k0, uint32_t sb) {
         k0 += kofs;
-        if (j < Lay::NX + 8) {
+        if (j < Lay::NX + Lay::NWC) {
             const bool isx = j < Lay::NX;
             const int q = isx ? j : j - Lay::NX;
             if (PASS2 && !isx) return;  // W is zero: its slabs were cleared once
-            const int blk = isx ? Lay::NX * wave + q : 8 * wave + q;
+            const int blk = isx ? Lay::NX * wave + q : Lay::NWC * wave + q;
             const uint32_t dst = sb + (isx ? Lay::X : Lay::W) + 1024 * blk;
             if constexpr (!RAGGED) {
                 copy16s_to_lds(uniform_ptr((isx ? Xt : Wt) + k0), isx ? offX[q] : offW[q], dst);
@@ -222,9 +231,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
                 const uint16_t* src = (isx ? Xt : Wt) + (int64_t)row * C + k0 + 8 * lc;
                 copy16_to_lds(ok ? (const void*)src : (const void*)zsrc, dst);
             }
-        } else if (j < Lay::NX + 8 + Lay::NAW) {
+        } else if (j < Lay::NX + Lay::NWC + Lay::NAW) {
             // every wave issues NAW copies; those past the A slab go to the sink
-            const int q = j - Lay::NX - 8, blk = 4 * q + wave;
+            const int q = j - Lay::NX - Lay::NWC, blk = 4 * q + wave;
             const bool has = blk < 2 * RK;
             const int row = 8 * blk + (lane >> 3);
             const int lc = (lane & 7) ^ tr64_swz(row);
@@ -232,12 +241,12 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             copy16_to_lds(ok ? (const void*)(aptr[q] + k0) : (const void*)zsrc,
                           has ? sb + Lay::A + 1024 * blk : lds0 + Lay::SINK);
         } else {
-            const int q = j - Lay::NX - 8 - Lay::NAW;
-            const uint32_t dst = sb + Lay::M + 256 * (2 * wave + q);
+            const int q = j - Lay::NX - Lay::NWC - Lay::NAW;
+            const uint32_t dst = sb + Lay::M + 256 * (Lay::NMC * wave + q);
             if constexpr (!RAGGED) {
                 copy4s_to_lds(uniform_ptr(Mt + (k0 >> 5)), offM[q], dst);
             } else {
-                const int e = 64 * (2 * wave + q) + lane;
+                const int e = 64 * (Lay::NMC * wave + q) + lane;
                 const bool ok = n0 + (e >> 1) < R && (k0 >> 5) + (e & 1) < wpr;
                 const uint32_t* src = Mt + (int64_t)(e >> 1) * wpr + (k0 >> 5) + (e & 1);
                 copy4_to_lds(ok ? (const void*)src : (const void*)zsrc, dst);
@@ -261,31 +270,31 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
                 offAt[kb][t] = Lay::A + tr64_elem_off(row, col);
             }
     }
-    const int nrow0 = 64 * wave + l32;
+    const int nrow0 = 32 * NF * wave + l32;
     auto xoff = [&](int mb, int c4) { return Lay::X + slab64_off(32 * mb + l32, 2 * c4 + h); };
     auto woff = [&](int nb, int c4) { return Lay::W + slab64_off(nrow0 + 32 * nb, 2 * c4 + h); };
 
-    f32x16 acc[MBW][2];
+    f32x16 acc[MBW][NF];
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NF; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
     bf16x8 xa[MBW], xb[MBW];  // X fragments of alternate sub-steps
-    u32x4 wa[2], wb[2];       // W' fragments of alternate sub-steps
-    f32x16 T[2];              // rank-r block of the current 32-wide k half
-    uint32_t mw[2][2];        // mask words [nb][kb] of the current K-step
-    u32x4 raw[2], sel[2];     // W and select masks of the sub-step being merged
-    u32x4 rwa[2], rwb[2];     // folded merge: W of the two sub-steps of a k half
+    u32x4 wa[NF], wb[NF];     // W' fragments of alternate sub-steps
+    f32x16 T[NF];             // rank-r block of the current 32-wide k half
+    uint32_t mw[NF][2];       // mask words [nb][kb] of the current K-step
+    u32x4 raw[NF], sel[NF];   // W and select masks of the sub-step being merged
+    u32x4 rwa[NF], rwb[NF];   // folded merge: W of the two sub-steps of a k half
     bf16x8 afr[RK];
 
     // MFMA slot i of a sub-step: token block i/2, feature block i%2 (the
-    // slots of token blocks a thin tile lacks are empty)
-    auto mm = [&](int i, const bf16x8 (&xf)[MBW], const u32x4 (&wf)[2]) {
+    // slots of token and feature blocks a thin tile lacks are empty)
+    auto mm = [&](int i, const bf16x8 (&xf)[MBW], const u32x4 (&wf)[NF]) {
         const int mb = i >> 1, nb = i & 1;
-        if (mb < MBW) acc[mb][nb] = mfma_32x32x16(xf[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
+        if (mb < MBW && nb < NF) acc[mb][nb] = mfma_32x32x16(xf[mb], as_bf16x8(wf[nb]), acc[mb][nb]);
     };
     auto read_afr = [&](const uint8_t* sb, int kb) {
 #pragma unroll
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     };
     auto read_mw = [&](const uint8_t* sb) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NF; ++nb) {
             const u32x2 v = *(const u32x2*)(sb + Lay::M + 8 * (nrow0 + 32 * nb));
             mw[nb][0] = v[0];
             mw[nb][1] = v[1];
@@ -304,7 +313,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     // raw W and select masks of sub-step c4 of the stage at sb
     auto read_rs = [&](const uint8_t* sb, int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NF; ++nb) {
             raw[nb] = *(const u32x4*)(sb + woff(nb, c4));
             sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
@@ -314,36 +323,39 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         if (2 * p + 1 < MBW) xf[2 * p + 1] = *(const bf16x8*)(sb + xoff(2 * p + 1, c4));
     };
     // merge piece p (0..7): pair p % 4 of fragment nb = p / 4, T half cp
-    auto merge_piece = [&](u32x4 (&wf)[2], int p, int cp) {
+    auto merge_piece = [&](u32x4 (&wf)[NF], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
-        wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
+        if (nb < NF)
+            wf[nb][q] = merge_pair(raw[nb][q], T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1], s, sel[nb][q]);
     };
     // folded merge: W of sub-step c4 (raw bf16 pairs), select masks of c4
-    auto read_raw = [&](u32x4 (&rw)[2], const uint8_t* sb, int c4) {
+    auto read_raw = [&](u32x4 (&rw)[NF], const uint8_t* sb, int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) rw[nb] = *(const u32x4*)(sb + woff(nb, c4));
+        for (int nb = 0; nb < NF; ++nb) rw[nb] = *(const u32x4*)(sb + woff(nb, c4));
     };
     auto read_sel = [&](int c4) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NF; ++nb) {
             sel[nb] = read_sel16(smem + Lay::LUT, mw[nb][c4 >> 1], 8 * (2 * (c4 & 1) + h));
         }
     };
     // pair p of rw, as fp32, into the accumulator half cp of the rank-r block
-    auto unpack = [&](const u32x4 (&rw)[2], int cp, int p) {
+    auto unpack = [&](const u32x4 (&rw)[NF], int cp, int p) {
         const int nb = p >> 2, q = p & 3;
-        T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
-        T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+        if (nb < NF) {
+            T[nb][8 * cp + 2 * q] = __uint_as_float(rw[nb][q] << 16);
+            T[nb][8 * cp + 2 * q + 1] = __uint_as_float(rw[nb][q] & 0xFFFF0000u);
+        }
     };
-    auto merge_fold = [&](u32x4 (&wf)[2], int p, int cp) {
+    auto merge_fold = [&](u32x4 (&wf)[NF], int p, int cp) {
         const int nb = p >> 2, q = p & 3;
-        wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
+        if (nb < NF) wf[nb][q] = pack_bf16x2(T[nb][8 * cp + 2 * q], T[nb][8 * cp + 2 * q + 1]) & sel[nb][q];
     };
     // an ordinary sub-step: MFMAs on (xc, wc) while preparing (xn, wn) for
     // sub-step c4n of the stage at sb; optionally the rank-r block of k half 1
-    // late_*: the copies kEarly.. of the stage in the other buffer, issued in
+    // late_*: the copies EARLY.. of the stage in the other buffer, issued in
     // the merge slots of the first sub-step of a K-step (see the main loop)
-    auto substep = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[2], bf16x8 (&xn)[MBW], u32x4 (&wn)[2],
+    auto substep = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[NF], bf16x8 (&xn)[MBW], u32x4 (&wn)[NF],
                        const uint8_t* sb, int c4n, auto rank_tag, int late_k = 0, uint32_t late_sq = 0,
                        bool late_on = false) {
         constexpr bool RANK = decltype(rank_tag)::value;
@@ -358,7 +370,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xc, wc);
             merge_piece(wn, p, c4n & 1);
-            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            if (late_on && Lay::EARLY + p < Lay::COPIES) copy_j(Lay::EARLY + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, xc, wc);
@@ -377,7 +389,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     //     of that stage have landed (no barrier needed: each wave copies the
     //     W rows it merges); the rank-r MFMAs of that k half run after the
     //     barrier.
-    auto substep_fold = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[2], bf16x8 (&xn)[MBW], u32x4 (&wn)[2],
+    auto substep_fold = [&](const bf16x8 (&xc)[MBW], const u32x4 (&wc)[NF], bf16x8 (&xn)[MBW], u32x4 (&wn)[NF],
                             const uint8_t* sb, const uint8_t* snext, int c4n, int late_k = 0,
                             uint32_t late_sq = 0, bool late_on = false) {
         const int cp = c4n & 1;
@@ -389,7 +401,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             read_x2(xn, sb, c4n, i);
             if (c4n == 1) { unpack(rwa, 0, 2 * i); unpack(rwa, 0, 2 * i + 1); }
             if (c4n == 3 && i == 3) {
-                wait_vmcnt<Lay::NAW + 2>();  // this wave's W copies of the next stage
+                wait_vmcnt<Lay::NAW + Lay::NMC>();  // this wave's W copies of the next stage
                 read_raw(rwa, snext, 0);
                 read_raw(rwb, snext, 1);
             }
@@ -402,7 +414,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
             merge_fold(wn, p, cp);
             if (c4n == 1) unpack(rwb, 1, p);
             if (c4n == 3) { unpack(rwb, 1, p); unpack(rwa, 0, p); }
-            if (late_on && kEarly + p < Lay::COPIES) copy_j(kEarly + p, late_k, late_sq);
+            if (late_on && Lay::EARLY + p < Lay::COPIES) copy_j(Lay::EARLY + p, late_k, late_sq);
             SLOT_END();
         }
         mm(15, xc, wc);
@@ -411,8 +423,8 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     };
 
     if constexpr (PASS2) {  // W taken as zero: clear both W slabs once, never copy them
-        for (int i = tid; i < 2 * (WB / 16); i += NT)
-            *(u32x4*)(smem + (i / (WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (WB / 16))) = zero_u32x4();
+        for (int i = tid; i < 2 * (Lay::WB / 16); i += NT)
+            *(u32x4*)(smem + (i / (Lay::WB / 16)) * Lay::STAGE + Lay::W + 16 * (i % (Lay::WB / 16))) = zero_u32x4();
         __syncthreads();
     }
 
@@ -453,7 +465,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const int st = kt & 1;
         const uint8_t* sb = smem + st * Lay::STAGE;
         const uint8_t* sn = smem + (st ^ 1) * Lay::STAGE;
-        // copies kEarly.. of stage kt+1 (buffer st^1, free since the last
+        // copies EARLY.. of stage kt+1 (buffer st^1, free since the last
         // barrier; the barrier below waits for them); at kt = 0 the prologue
         // issued all of stage 1
         const int k1 = (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
@@ -472,41 +484,44 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
         const uint32_t sq = lds0 + st * Lay::STAGE;
         // one copy per MFMA slot: a copy issued behind an MFMA stalls the
         // wave while that MFMA runs, a second one would stall the next
-        mm(0, xb, wb); read_mw(sn); read_afr(sn, 0); copy_j(0, k2, sq); SLOT_END();
-        mm(1, xb, wb); copy_j(1, k2, sq); SLOT_END();
-        mm(2, xb, wb); read_x2(xa, sn, 0, 0); copy_j(2, k2, sq); SLOT_END();
-        mm(3, xb, wb); read_x2(xa, sn, 0, 1); copy_j(3, k2, sq); SLOT_END();
+        auto early = [&](int j) {
+            if (j < Lay::EARLY) copy_j(j, k2, sq);
+        };
+        mm(0, xb, wb); read_mw(sn); read_afr(sn, 0); early(0); SLOT_END();
+        mm(1, xb, wb); early(1); SLOT_END();
+        mm(2, xb, wb); read_x2(xa, sn, 0, 0); early(2); SLOT_END();
+        mm(3, xb, wb); read_x2(xa, sn, 0, 1); early(3); SLOT_END();
         mm(4, xb, wb);
         if constexpr (FOLD) read_sel(0);
         else read_rs(sn, 0);
-        copy_j(4, k2, sq); SLOT_END();
-        mm(5, xb, wb); read_x2(xa, sn, 0, 2); copy_j(5, k2, sq); SLOT_END();
+        early(4); SLOT_END();
+        mm(5, xb, wb); read_x2(xa, sn, 0, 2); early(5); SLOT_END();
         mm(6, xb, wb); read_x2(xa, sn, 0, 3);
         if constexpr (FOLD) rank_mfma2_acc<RK>(T, afr, bfr);
         else rank_mfma2<RK>(T, afr, bfr);
-        copy_j(6, k2, sq); SLOT_END();
+        early(6); SLOT_END();
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             mm(7 + p, xb, wb);
             if constexpr (FOLD) merge_fold(wa, p, 0);
             else merge_piece(wa, p, 0);
-            if (7 + p < kEarly) copy_j(7 + p, k2, sq);
+            early(7 + p);
             SLOT_END();
         }
         mm(15, xb, wb);
         SLOT_END();
     }
-    // ---- epilogue: (+bias), round to bf16, stage the wave's TM x 64 block in
-    // LDS (rows of 64 outputs, 128 B), then 16-byte stores of whole rows.
+    // ---- epilogue: (+bias), round to bf16, stage the wave's TM x 32 NF block
+    // in LDS (rows of 32 NF outputs), then 16-byte stores of whole rows.
     wait_vmcnt<0>();
     lds_barrier();  // every wave's copies landed and every read of the stages done
-    if (TM == BM && (int)blockIdx.x >= n_full) {
+    if (TM == BM && NF == 2 && (int)blockIdx.x >= n_full) {
         // a piece of a split tile: its unrounded fp32 partial sums go to slice
         // blockIdx.x - n_full of `part` (256 tokens x 256 features); the
         // reduction launch adds the pieces in order, adds the bias and rounds
         float* dst = part + (int64_t)((int)blockIdx.x - n_full) * (BM * BN);
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
             for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
@@ -514,23 +529,25 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
                     dst[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * BN + nrow0 + 32 * nb] = acc[mb][nb][v];
         return;
     }
-    uint16_t* ol = (uint16_t*)(smem + wave * (TM * 128));
+    constexpr int OW = 32 * NF;   // outputs per staged row
+    constexpr int CH = OW / 8;    // 16-byte chunks per row
+    uint16_t* ol = (uint16_t*)(smem + wave * (TM * OW * 2));
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NF; ++nb) {
         const int gn = n0 + nrow0 + 32 * nb;
         const float bv = (bias != nullptr && gn < R) ? bf16_bits_to_f32(bias[gn]) : 0.f;
 #pragma unroll
         for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
-                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * nb + l32] = bf16_bits(acc[mb][nb][v] + bv);
+                ol[(32 * mb + 8 * (v >> 2) + 4 * h + (v & 3)) * OW + 32 * nb + l32] = bf16_bits(acc[mb][nb][v] + bv);
     }
 #pragma unroll 4
-    for (int it = 0; it < TM / 8; ++it) {
-        const int row = 8 * it + (lane >> 3), ch = lane & 7;
-        const u32x4 v = *(const u32x4*)(ol + row * 64 + 8 * ch);
+    for (int it = 0; it < TM * CH / 64; ++it) {
+        const int row = (64 / CH) * it + lane / CH, ch = lane % CH;
+        const u32x4 v = *(const u32x4*)(ol + row * OW + 8 * ch);
         const int64_t gm = m0 + row;
-        const int gn = n0 + 64 * wave + 8 * ch;
+        const int gn = n0 + OW * wave + 8 * ch;
         if (gm < L && gn < R) {
             if constexpr (PASS2)
                 *(u32x4*)(Y + gm * R + gn) = add_bf16x8(*(const u32x4*)(Y + gm * R + gn), v);
@@ -553,7 +570,7 @@ bool power_of_two(float s) {
 template <int RK, bool TWO_FOUR, bool RAGGED, bool PASS2, bool FOLD>
 void launch_whole(const LayerArgs& a, hipStream_t st, int ldb, int grid, int tiles_m, int tiles_n, int n_full,
                   int split, float* part) {
-    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, RAGGED, PASS2, FOLD, BM>), dim3(grid), dim3(NT), 0, st,
+    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, RAGGED, PASS2, FOLD, BM, 2>), dim3(grid), dim3(NT), 0, st,
                        (const uint16_t*)a.X, (const uint16_t*)a.W, a.M, (const uint16_t*)a.B,
                        (const uint16_t*)a.A, (const uint16_t*)a.bias, (uint16_t*)a.Y, a.L, (int)a.R, (int)a.C,
                        (int)a.r, a.scale, tiles_m, tiles_n, ldb, n_full, split, part);
@@ -619,11 +636,12 @@ hipError_t launch_ranks(const LayerArgs& a, hipStream_t st, bool pass2, int ldb)
 
 #else  // LORS_THIN_TILES
 
+// thin tiles of one feature half (NF = 1) and TM tokens: 2 BM / TM per tile
 template <int RK, bool TWO_FOUR, bool FOLD, int TM>
 hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail) {
     const int tiles_m = (int)((a.L + BM - 1) / BM);
     const int tiles_n = (int)((a.R + BN - 1) / BN);
-    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, false, FOLD, TM>), dim3(tail * (BM / TM)), dim3(NT), 0, st,
+    hipLaunchKernelGGL((fwd_kernel<RK, TWO_FOUR, false, false, FOLD, TM, 1>), dim3(tail * (2 * BM / TM)), dim3(NT), 0, st,
                        (const uint16_t*)a.X, (const uint16_t*)a.W, a.M, (const uint16_t*)a.B,
                        (const uint16_t*)a.A, (const uint16_t*)a.bias, (uint16_t*)a.Y, a.L, (int)a.R, (int)a.C,
                        (int)a.r, a.scale, tiles_m, tiles_n, ldb, first, tail, (float*)nullptr);
@@ -632,10 +650,10 @@ hipError_t launch_thin_tm(const LayerArgs& a, hipStream_t st, int ldb, int first
 
 template <int RK, bool TWO_FOUR, bool FOLD>
 hipError_t launch_thin_q(const LayerArgs& a, hipStream_t st, int ldb, int first, int tail, int q) {
-    switch (q) {
-        case 2: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 2>(a, st, ldb, first, tail);
-        case 4: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 4>(a, st, ldb, first, tail);
-        case 8: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 8>(a, st, ldb, first, tail);
+    switch (q) {  // q thin tiles per tile: two feature halves, each cut into q/2 token parts
+        case 2: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM>(a, st, ldb, first, tail);
+        case 4: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 2>(a, st, ldb, first, tail);
+        case 8: return launch_thin_tm<RK, TWO_FOUR, FOLD, BM / 4>(a, st, ldb, first, tail);
         default: return hipErrorInvalidValue;
     }
 }

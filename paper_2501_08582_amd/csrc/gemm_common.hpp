@@ -170,33 +170,53 @@ __device__ __forceinline__ void copy4s_to_lds(const void* sbase, uint32_t voff, 
                  : "memory", "m0");
 }
 
-// T[nb] = sum over c of mfma(a[c], b[nb][c]) for nb = 0, 1, with T in VGPRs.
+// The wait states after the rank-r MFMA chains (see rank_mfma2): they cover
+// the matrix-result -> VALU-read latency of T and keep the A fragments
+// allocated until the matrix core has consumed them.
+template <int RK, int NB>
+__device__ __forceinline__ void rank_wait(f32x16 (&T)[NB], const bf16x8 (&a)[RK]) {
+    static_assert(NB == 1 || NB == 2, "one or two 32-wide blocks");
+    static_assert(RK >= 1 && RK <= 4, "ranks up to 64");
+    if constexpr (NB == 2) {
+        if constexpr (RK == 1)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]));
+        else if constexpr (RK == 2)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]));
+        else if constexpr (RK == 3)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
+        else
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2"
+                         : "+v"(T[0]), "+v"(T[1])
+                         : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+    } else {
+        if constexpr (RK == 1)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]) : "v"(a[0]));
+        else if constexpr (RK == 2)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]) : "v"(a[0]), "v"(a[1]));
+        else if constexpr (RK == 3)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
+        else
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]) : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+    }
+}
+
+// T[nb] = sum over c of mfma(a[c], b[nb][c]) for nb < NB (two 32-wide blocks,
+// or one for a tile of half the features), with T in VGPRs.
 // The main accumulators fill the accumulation registers, so results that the
 // VALU consumes are produced by inline-assembly MFMAs writing VGPRs directly
 // (chained accumulation into the same registers needs no wait states).  The
 // final s_nop block covers the matrix-result -> VALU-read latency; it also
 // keeps the A fragments allocated until the matrix core has consumed them.
-template <int RK>
-__device__ __forceinline__ void rank_mfma2(f32x16 (&T)[2], const bf16x8 (&a)[RK], const bf16x8 (&b)[2][RK]) {
+template <int RK, int NB>
+__device__ __forceinline__ void rank_mfma2(f32x16 (&T)[NB], const bf16x8 (&a)[RK], const bf16x8 (&b)[NB][RK]) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
         asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(T[nb]) : "v"(a[0]), "v"(b[nb][0]));
 #pragma unroll
         for (int c = 1; c < RK; ++c)
             asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[c]), "v"(b[nb][c]));
     }
-    if constexpr (RK == 1)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]));
-    else if constexpr (RK == 2)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]));
-    else if constexpr (RK == 3)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
-    else {
-        static_assert(RK == 4, "ranks up to 64");
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2"
-                     : "+v"(T[0]), "+v"(T[1])
-                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
-    }
+    rank_wait<RK, NB>(T, a);
 }
 
 // The same products accumulated onto T: T[nb] += sum over c of
@@ -204,27 +224,16 @@ __device__ __forceinline__ void rank_mfma2(f32x16 (&T)[2], const bf16x8 (&a)[RK]
 // holds W when the merge folds W into the matrix product), so each chain
 // starts with wait states that cover a VALU write -> matrix source-C read,
 // which the compiler cannot see through inline assembly.
-template <int RK>
-__device__ __forceinline__ void rank_mfma2_acc(f32x16 (&T)[2], const bf16x8 (&a)[RK], const bf16x8 (&b)[2][RK]) {
+template <int RK, int NB>
+__device__ __forceinline__ void rank_mfma2_acc(f32x16 (&T)[NB], const bf16x8 (&a)[RK], const bf16x8 (&b)[NB][RK]) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
         asm volatile("s_nop 4\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[0]), "v"(b[nb][0]));
 #pragma unroll
         for (int c = 1; c < RK; ++c)
             asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+&v"(T[nb]) : "v"(a[c]), "v"(b[nb][c]));
     }
-    if constexpr (RK == 1)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]));
-    else if constexpr (RK == 2)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]));
-    else if constexpr (RK == 3)
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2" : "+v"(T[0]), "+v"(T[1]) : "v"(a[0]), "v"(a[1]), "v"(a[2]));
-    else {
-        static_assert(RK == 4, "ranks up to 64");
-        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 2"
-                     : "+v"(T[0]), "+v"(T[1])
-                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
-    }
+    rank_wait<RK, NB>(T, a);
 }
 
 // One bf16 pair of W' = select(M, W + s.T, 0): raw holds the two bf16 of W,

@@ -53,13 +53,15 @@ TailSplit tail_split(int64_t tiles, int64_t nk, int64_t max_part_bytes);
 inline int64_t split_part_bytes(const TailSplit& t) {
     return t.split > 1 ? (int64_t)(t.grid - t.n_full) * kPieceBytes : 0;
 }
-// A short last wave of 256 x 256 tiles cut over its tokens instead: each of
-// its `tail` tiles becomes q thin tiles of 256/q tokens and all 256 output
-// features (q = 2, 4 or 8, as many as fill the CUs; q = 1: not cut).  A thin
-// tile runs the whole K-loop with the same per-element arithmetic as a whole
-// tile, so its results are the same bits, and it needs no workspace; it
-// merges the same W' rows, so a thin tile costs more than 1/q of a whole one.
-// Applies to a wave that fills at most half of the CUs, like tail_split.
+// A short last wave of 256 x 256 tiles cut into thin tiles instead: each of
+// its `tail` tiles becomes q thin tiles (q = 2, 4 or 8, as many as fill the
+// CUs; q = 1: not cut) -- its two halves of 128 output features, each cut
+// over the tokens into q/2 parts of 512/q tokens.  A thin tile runs the whole
+// K-loop with the same per-element arithmetic as a whole tile, so its
+// results are the same bits, and it needs no workspace.  Its waves merge 32
+// rows of W' each instead of 64, so the merge shrinks with the tile, though
+// less than the matrix work does when the tokens are cut too.  Applies to a
+// wave that fills at most half of the CUs, like tail_split.
 // n_full: the tiles that run whole (the first n_full in the kernels' order).
 struct ThinPlan {
     int n_full, tail, q;
