@@ -292,7 +292,7 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
     bf16x8 afr[NF][RK];       // A[16c + 8h .. +7][n] (scaled by s when the merge is folded)
 
     // MFMA slot i of a sub-step: token block i/2, feature block i%2 (the
-    // slots of token blocks a thin tile lacks are empty)
+    // slots of token and feature blocks a thin tile lacks are empty)
     auto mm = [&](int i, const bf16x8 (&df)[MBW], const u32x4 (&wf)[NF]) {
         const int mb = i >> 1, nb = i & 1;
         if (mb < MBW && nb < NF) acc[mb][nb] = mfma_32x32x16(df[mb], as_bf16x8(wf[nb]), acc[mb][nb]);

@@ -1,6 +1,7 @@
 // Thin-tile instances of the forward kernel: the tiles of a short last wave,
-// each cut over its tokens (see thin_plan in kernels.hpp).  The kernel is the
-// one in fwd_bf16.hip; this unit instantiates only its thin forms, so that
-// they compile in parallel with the whole-tile ones.
+// each cut into feature halves and token parts (see thin_plan in
+// kernels.hpp).  The kernel is the one in fwd_bf16.hip; this unit
+// instantiates only its thin forms, so that they compile in parallel with the
+// whole-tile ones.
 #define LORS_THIN_TILES 1
 #include "fwd_bf16.hip"
