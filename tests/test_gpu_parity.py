@@ -454,7 +454,7 @@ def test_parity_rank_bucket_edges(R, C, L, r, mask):
     (520, 776, 300, 96, "magnitude"),   # ragged, second pass r = 32
     (264, 1032, 77, 72, "2:4"),         # second pass r = 8
     (768, 512, 513, 128, "magnitude"),  # second pass r = 64, one token past a tile
-    (512, 768, 512, 80, "2:4"),         # whole tiles (fixed-offset copies)
+    (512, 768, 512, 80, "2:4"),         # whole tiles: the first pass as thin tiles, the second whole
 ])
 def test_parity_two_pass_ranks(R, C, L, r, mask):
     name = "llama2_7b_up_proj_2_4" if mask == "2:4" else "llama2_7b_q_proj"
