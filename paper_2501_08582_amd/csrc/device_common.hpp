@@ -139,6 +139,18 @@ __device__ __forceinline__ void thin_coords(int bid, int tiles_m, int tiles_n, i
     group_coords(first + i, tiles_m, tiles_n, group_m, tm, tn);
 }
 
+// Index of word iw (rows 32 iw .. 32 iw + 31 of R) of column col in the
+// transposed mask M^T (C columns, wprT words each).  M^T is stored K-step-major:
+// the two words of each aligned pair (2p, 2p + 1) -- the 64 rows of R that
+// one K-step of dX covers -- form one block, column after column, so the
+// columns of a dX tile read one contiguous run per K-step; with an odd word
+// count the last word forms a block of width 1.
+__device__ __forceinline__ int64_t mt_index(int64_t col, int iw, int64_t C, int wprT) {
+    const int p2 = iw & ~1;
+    const int width = min(2, wprT - p2);
+    return (int64_t)p2 * C + col * width + (iw - p2);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ u32x4 zero_u32x4() { return u32x4{0u, 0u, 0u, 0u}; }

@@ -197,15 +197,15 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             offW[q] = (uint32_t)((rw * C + 32 * wave + 8 * (lane & 3)) * 2);
         }
     }
+    // M^T words of a K-step: with whole tiles the tile's columns hold them
+    // as one contiguous run of 2 words per column (see mt_index), so copy q
+    // of a wave moves 256 consecutive bytes of it
     uint32_t offM[Lay::NMC];
 #pragma unroll
-    for (int q = 0; q < Lay::NMC; ++q) {
-        const int e = 64 * (Lay::NMC * wave + q) + lane;
-        offM[q] = (uint32_t)(((e >> 1) * wprT + (e & 1)) * 4);
-    }
+    for (int q = 0; q < Lay::NMC; ++q) offM[q] = (uint32_t)((64 * (Lay::NMC * wave + q) + lane) * 4);
     const uint16_t* Dt = uniform_ptr(dY + m0 * R);
     const uint16_t* Wn = uniform_ptr(W + n0);
-    const uint32_t* Mn = uniform_ptr(Mt + (int64_t)n0 * wprT);
+    const uint32_t* Mn = uniform_ptr(Mt + 2 * (int64_t)n0);
 
     auto copy_j = [&](int j, int k0, uint32_t sb) {
         k0 += kofs;
@@ -244,12 +244,12 @@ __global__ __launch_bounds__(NT, 1) void dx_kernel(
             const int q = j - Lay::ND - Lay::NWC - Lay::NB;
             const uint32_t dst = sb + Lay::M + 256 * (Lay::NMC * wave + q);
             if constexpr (!RAGGED) {
-                copy4s_to_lds(uniform_ptr(Mn + (k0 >> 5)), offM[q], dst);
+                copy4s_to_lds(uniform_ptr(Mn + (int64_t)(k0 >> 5) * C), offM[q], dst);
             } else {
                 const int e = 64 * (Lay::NMC * wave + q) + lane;
                 const int n = e >> 1, gw = (k0 >> 5) + (e & 1);
                 const bool ok = n0 + n < C && gw < wprT;
-                copy4_to_lds(ok ? (const void*)(Mn + (int64_t)n * wprT + gw) : (const void*)zsrc, dst);
+                copy4_to_lds(ok ? (const void*)(Mt + mt_index(n0 + n, gw, C, wprT)) : (const void*)zsrc, dst);
             }
         }
     };

@@ -236,7 +236,7 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
         const int e = 64 * blk + lane;
         const int j = e >> 3, iw = e & 7;
         const int gj = j0 + j, giw = (i0 >> 5) + iw;
-        copy4_to_lds((gj < C && giw < wprT) ? (const void*)(Mt + (int64_t)gj * wprT + giw) : (const void*)zsrc,
+        copy4_to_lds((gj < C && giw < wprT) ? (const void*)(Mt + mt_index(gj, giw, C, wprT)) : (const void*)zsrc,
                      lds0 + EP_MT + 256 * blk);
     }
     auto copy_a_block = [&](int jb) {  // A[32jb .. +31][j0 .. j0+255] -> EP_A

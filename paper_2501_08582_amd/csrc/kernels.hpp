@@ -15,7 +15,7 @@ struct LayerArgs {
     const void* X;          // L x C
     const void* W;          // R x C
     const uint32_t* M;      // R x ceil(C/32), the caller's layout
-    const uint32_t* Mt;     // C x ceil(R/32) transposed bitmap (backward only)
+    const uint32_t* Mt;     // C x ceil(R/32) transposed bitmap, K-step-major (mt_index; backward only)
     bool reuse_mt;          // Mt already holds the transposed mask
     const void* B;          // R x r
     const void* A;          // r x C
@@ -76,9 +76,7 @@ inline bool fwd_whole_tiles(int64_t L, int64_t R, int64_t C) {
     return L % 256 == 0 && R % 256 == 0 && C % 64 == 0 && 256 * C * 2 < (1ll << 31);
 }
 inline bool dx_whole_tiles(int64_t L, int64_t R, int64_t C) {
-    const int64_t wprT = (R + 31) / 32;
-    return L % 256 == 0 && C % 256 == 0 && R % 64 == 0 && 256 * R * 2 < (1ll << 31) && 64 * C * 2 < (1ll << 31) &&
-           256 * wprT * 4 < (1ll << 31);
+    return L % 256 == 0 && C % 256 == 0 && R % 64 == 0 && 256 * R * 2 < (1ll << 31) && 64 * C * 2 < (1ll << 31);
 }
 // out (rows x cols, bf16) on the split tiles = the sum of their pieces'
 // partials in piece order (+ bias[col] when bias is not null), rounded once.

@@ -121,8 +121,8 @@ __global__ __launch_bounds__(NT) void unpack_kernel(const uint32_t* __restrict__
     for (int e = 0; e < 32 && c0 + e < C; ++e) row[c0 + e] = (uint8_t)keep1<TWO_FOUR>(word, (uint32_t)e);
 }
 
-// Transposed bitmap: one wave handles a 32-row block of the mask and two
-// 32-column words.  Lane l < 32 reads row 32*iw + l of word jw, lane l >= 32
+// Transposed bitmap (K-step-major, see mt_index): one wave handles a 32-row
+// block of the mask and two 32-column words.  Lane l < 32 reads row 32*iw + l of word jw, lane l >= 32
 // the same row of word jw + 1 (2:4 codes are first expanded to keep bits);
 // one ballot per bit position then yields, for every column, its 32 keep bits.
 template <bool TWO_FOUR>
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(NT) void transpose_kernel(const uint32_t* __restric
         mine = ((lane & 31) == b) ? (lane < 32 ? lo : hi) : mine;
     }
     const int64_t col = (int64_t)32 * jw + (lane & 31);
-    if (jw < wpr && col < C) out[col * wprT + iw] = mine;
+    if (jw < wpr && col < C) out[mt_index(col, (int)iw, C, wprT)] = mine;
 }
 
 __global__ __launch_bounds__(NT) void zero_kernel(float* __restrict__ p, int64_t n) {

@@ -57,9 +57,7 @@ def fwd_whole_tiles(L, R, C):
 
 def dx_whole_tiles(L, R, C):
     """The same for dX: tiles over L x C, K-steps over R."""
-    wprT = -(-R // 32)
-    return (L % 256 == 0 and C % 256 == 0 and R % 64 == 0 and 256 * R * 2 < 2**31 and 64 * C * 2 < 2**31
-            and 256 * wprT * 4 < 2**31)
+    return L % 256 == 0 and C % 256 == 0 and R % 64 == 0 and 256 * R * 2 < 2**31 and 64 * C * 2 < 2**31
 
 
 def thin_q(tiles, cus=256):
