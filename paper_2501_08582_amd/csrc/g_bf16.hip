@@ -41,8 +41,8 @@ constexpr int GT_PITCH = 512;                      // G^T tile: [j][i], 256 i pe
 constexpr int GT_BYTES = BN * GT_PITCH;            // 128 KiB
 constexpr int EP_MT = 0;                           // M^T words [j][8]: 8 KiB
 constexpr int EP_LUT = 8192;                       // select LUT: 4 KiB
-constexpr int EP_B = 12288;                        // B block [i][32*JB] bf16: up to 64 KiB
-constexpr int EP_X = 12288 + BM * 64 * 4;           // dA exchange [2][16][64] fp32: 8 KiB (after the largest B block)
+constexpr int EP_B = 12288;                        // B block [i][32*JB] bf16: 16 KiB per 32 ranks
+                                                   // (then the dA exchange, see the kernel)
 constexpr int EP_A = SMEM;                         // A block [32 j'][256 j]: 16 KiB
 constexpr int SMEM_ALL = SMEM + 32 * kRowBytes;
 
@@ -56,8 +56,12 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
     const uint16_t* __restrict__ Am, float* __restrict__ dB, float* __restrict__ dA,
     int64_t L, int R, int C, int r, float s, int tiles_m, int tiles_n, int n_full, int split) {
     constexpr int JB = (RK + 1) / 2;  // 32-wide blocks of the rank
+    // dA exchange: JBC rank blocks per round, one 4 KiB slot [v/4][lane][4]
+    // per (wj, column block b, rank block of the round), right after the B block
+    constexpr int JBC = JB <= 2 ? JB : 1;
+    constexpr int EP_X = EP_B + BM * 32 * JB * 2;
     static_assert(GT_BYTES <= SMEM, "G^T tile fits");
-    static_assert(EP_B + BM * 32 * JB * 2 <= EP_X && EP_X + 2 * 16 * kWave * 4 <= SMEM, "B block and dA exchange fit");
+    static_assert(EP_X + 2 * 4 * JBC * 16 * kWave * 4 <= SMEM, "B block and dA exchange fit");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM_ALL];
 
     const int tid = threadIdx.x;
@@ -298,52 +302,76 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
 
     // ---- epilogue 3: dA[j'][j] += s * sum_i B[i][j'] G[i][j], with the masked
     // bf16 accumulators as the MFMA B operand (K = rows i in accumulator
-    // order); the A operand B^T comes from the B block by transpose loads.
+    // order); the A operand B^T comes from the B block by transpose loads, one
+    // fragment per (row block, rank block) shared by the four column blocks b.
     // The two waves with the same wj hold partial sums over the two halves of
-    // the tile's rows: for column blocks b = 0, 1 wave wi = 1 hands its partial
+    // the tile's rows: for column blocks b = 0, 1 wave wi = 1 hands its partials
     // to wave wi = 0 through LDS, for b = 2, 3 the other way round, so each dA
-    // element receives one atomic add per tile.
+    // element receives one atomic add per tile.  All partials of a round are
+    // formed first, then exchanged behind one barrier.
     {
         const int g = lane >> 4, jj = lane & 15;
-        float* xch = (float*)(smem + EP_X) + wj * 16 * kWave;  // [wj][v][lane]
+        auto slot = [&](int b, int jl) {
+            return (u32x4*)(smem + EP_X) + ((wj * 4 + b) * JBC + jl) * 4 * kWave;
+        };
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int gj = j0 + wj * 128 + 32 * b + l32;
-            const bool giver = (b < 2) == (wi == 1);
+        for (int jb0 = 0; jb0 < JB; jb0 += JBC) {
+            f32x16 part[4][JBC];
 #pragma unroll
-            for (int jb = 0; jb < JB; ++jb) {
-                f32x16 da;
+            for (int b = 0; b < 4; ++b)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) da[v] = 0.f;
-                const int col = 32 * jb + 16 * (g & 1) + 4 * (jj & 3);
+                for (int jl = 0; jl < JBC; ++jl)
 #pragma unroll
-                for (int a = 0; a < 4; ++a) {
+                    for (int v = 0; v < 16; ++v) part[b][jl][v] = 0.f;
+#pragma unroll
+            for (int jl = 0; jl < JBC; ++jl) {
+                const int col = 32 * (jb0 + jl) + 16 * (g & 1) + 4 * (jj & 3);
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
 #pragma unroll
                     for (int c = 0; c < 2; ++c) {
                         const int row = wi * 128 + 32 * a + 16 * c + 4 * (g >> 1) + (jj >> 2);
-                        const u32x2 lo = lds_tr_read(smem + EP_B + 2 * (row * 32 * JB + col));
-                        const u32x2 hi = lds_tr_read(smem + EP_B + 2 * ((row + 8) * 32 * JB + col));
-                        da = mfma_32x32x16(frag_from_tr(lo, hi), as_bf16x8(gb[a][b][c]), da);
+                        const bf16x8 bt = frag_from_tr(lds_tr_read(smem + EP_B + 2 * (row * 32 * JB + col)),
+                                                       lds_tr_read(smem + EP_B + 2 * ((row + 8) * 32 * JB + col)));
+#pragma unroll
+                        for (int b = 0; b < 4; ++b) part[b][jl] = mfma_32x32x16(bt, as_bf16x8(gb[a][b][c]), part[b][jl]);
                     }
+            }
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                if ((b < 2) == (wi == 1)) {  // giver
+#pragma unroll
+                    for (int jl = 0; jl < JBC; ++jl)
+#pragma unroll
+                        for (int v4 = 0; v4 < 4; ++v4)
+                            slot(b, jl)[v4 * kWave + lane] = u32x4{__float_as_uint(part[b][jl][4 * v4]),
+                                                                   __float_as_uint(part[b][jl][4 * v4 + 1]),
+                                                                   __float_as_uint(part[b][jl][4 * v4 + 2]),
+                                                                   __float_as_uint(part[b][jl][4 * v4 + 3])};
                 }
-                if (giver) {
+            lds_barrier();
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) xch[v * kWave + lane] = da[v];
-                }
-                lds_barrier();
-                if (!giver) {
+            for (int b = 0; b < 4; ++b)
+                if ((b < 2) == (wi == 0)) {  // receiver
+                    const int gj = j0 + wj * 128 + 32 * b + l32;
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) da[v] += xch[v * kWave + lane];
-                    if (gj < C) {
+                    for (int jl = 0; jl < JBC; ++jl) {
 #pragma unroll
-                        for (int v = 0; v < 16; ++v) {
-                            const int jr = 32 * jb + 8 * (v >> 2) + 4 * h + (v & 3);
-                            if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * da[v]);
+                        for (int v4 = 0; v4 < 4; ++v4) {
+                            const u32x4 o = slot(b, jl)[v4 * kWave + lane];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) part[b][jl][4 * v4 + e] += __uint_as_float(o[e]);
+                        }
+                        if (gj < C) {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v) {
+                                const int jr = 32 * (jb0 + jl) + 8 * (v >> 2) + 4 * h + (v & 3);
+                                if (jr < r) atomicAdd(dA + (int64_t)jr * C + gj, s * part[b][jl][v]);
+                            }
                         }
                     }
                 }
-                lds_barrier();  // exchange slot free again
-            }
+            lds_barrier();  // exchange slots free again (and, after the last round, for G^T)
         }
     }
 
