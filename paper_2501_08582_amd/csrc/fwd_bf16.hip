@@ -433,7 +433,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_kernel(
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, 0, lds0);
 #pragma unroll
     for (int j = 0; j < Lay::COPIES; ++j) copy_j(j, nk > 1 ? BK : 0, lds0 + Lay::STAGE);
-    stage_barrier<0>();
+    // stage 0 landed everywhere (stage 1's copies, the last issued, may still
+    // fly: the first K-step's barrier waits for them)
+    stage_barrier<PASS2 ? Lay::COPIES - Lay::NWC : Lay::COPIES>();
     read_mw(smem);
     read_afr(smem, 0);
     if constexpr (FOLD) {

@@ -399,33 +399,37 @@ __global__ __launch_bounds__(NT, 1) void g_kernel(
 
     // ---- epilogue 5: dB[i][j'] += s * sum_j G[i][j] A[j'][j], one 32-wide
     // rank block at a time: A[32jb .. +31][j0 .. j0+255] is copied to LDS and
-    // wave w accumulates rows i = 64w .. 64w+63 of the tile.
+    // wave w accumulates rows i = 64w .. 64w+63 of the tile, both 32-row blocks
+    // together (each A fragment read once for the two).
     for (int jb = 0; jb < JB; ++jb) {
         if (jb > 0) copy_a_block(jb);  // block 0 was requested with the side data
         stage_barrier<0>();  // A block landed; G^T complete
+        const int g = lane >> 4, jj = lane & 15;
+        f32x16 db[2];
 #pragma unroll
-        for (int ib = 0; ib < 2; ++ib) {
-            const int irow0 = 64 * wave + 32 * ib;
-            f32x16 db;
+        for (int ib = 0; ib < 2; ++ib)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) db[v] = 0.f;
-            const int g = lane >> 4, jj = lane & 15;
+            for (int v = 0; v < 16; ++v) db[ib][v] = 0.f;
 #pragma unroll 4
-            for (int kc = 0; kc < BN / 16; ++kc) {
-                const int jr0 = 16 * kc + 8 * (g >> 1) + (jj >> 2);
-                const int ic = irow0 + 16 * (g & 1) + 4 * (jj & 3);
+        for (int kc = 0; kc < BN / 16; ++kc) {
+            const int jr0 = 16 * kc + 8 * (g >> 1) + (jj >> 2);
+            const bf16x8 av = *(const bf16x8*)(smem + EP_A + tile_off(l32, 16 * kc + 8 * h));
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib) {
+                const int ic = 64 * wave + 32 * ib + 16 * (g & 1) + 4 * (jj & 3);
                 const bf16x8 ga = frag_from_tr(lds_tr_read(smem + gt_off(jr0, ic)), lds_tr_read(smem + gt_off(jr0 + 4, ic)));
-                const bf16x8 av = *(const bf16x8*)(smem + EP_A + tile_off(l32, 16 * kc + 8 * h));
-                db = mfma_32x32x16(ga, av, db);
+                db[ib] = mfma_32x32x16(ga, av, db[ib]);
             }
-            const int jr = 32 * jb + l32;
-            if (jr < r) {
+        }
+        const int jr = 32 * jb + l32;
+        if (jr < r) {
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int gi = i0 + irow0 + 8 * (v >> 2) + 4 * h + (v & 3);
-                    if (gi < R) atomicAdd(dB + (int64_t)gi * r + jr, s * db[v]);
+                    const int gi = i0 + 64 * wave + 32 * ib + 8 * (v >> 2) + 4 * h + (v & 3);
+                    if (gi < R) atomicAdd(dB + (int64_t)gi * r + jr, s * db[ib][v]);
                 }
-            }
         }
         lds_barrier();  // A block free for the next rank block
     }
