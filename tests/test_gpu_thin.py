@@ -1,10 +1,11 @@
 """Thin tiles of a short last wave (forward and dX, whole-tile shapes).
 
 When a grid of 256 x 256 output tiles ends in a wave that fills at most half
-of the CUs, the library cuts each of its tiles over the tokens into 2, 4 or 8
-thin tiles (as many as fit on the CUs).  A thin tile runs the same arithmetic
-for each output element as a whole tile -- the whole K-loop, the same
-merge of W' and the same MFMA order -- so:
+of the CUs, the library cuts each of its tiles into 2, 4 or 8 thin tiles (as
+many as fit on the CUs): its two halves of 128 output features, each cut over
+the tokens into 1, 2 or 4 parts.  A thin tile runs the same arithmetic for
+each output element as a whole tile -- the whole K-loop, the same merge of W'
+and the same MFMA order -- so:
 
   * an output block computed in a thin tile equals, bit for bit, the same
     block computed in a whole tile.  Each case has one 256-token tile row
@@ -90,8 +91,9 @@ def test_thin_tiles_match_whole_tiles_and_the_oracle(kind, t, r, mask, scale, bi
     # for its last t blocks (cus .. cus+t-1 after the rotation)
     assert np.array_equal(out[:, 256 * (cus - t):256 * cus], rot[:, thin_cols])
 
-    # oracle, on sampled entries of every thin tile: 16 tokens of each thin
-    # tile's token range x 32 features
+    # oracle, on sampled entries of every thin tile: tokens from each of q
+    # token ranges (finer than the thin tiles' token parts) x 32 features of
+    # the block, which cover both feature halves
     rng = np.random.default_rng(t + r)
     f = lambda a: to_f64(a, "bf16")  # noqa: E731
     b64 = f(bias_bits) if bias else None
