@@ -122,9 +122,10 @@ __global__ __launch_bounds__(NT) void unpack_kernel(const uint32_t* __restrict__
 }
 
 // Transposed bitmap (K-step-major, see mt_index): one wave handles a 32-row
-// block of the mask and two 32-column words.  Lane l < 32 reads row 32*iw + l of word jw, lane l >= 32
-// the same row of word jw + 1 (2:4 codes are first expanded to keep bits);
-// one ballot per bit position then yields, for every column, its 32 keep bits.
+// block of the mask and two 32-column words.  Lane l < 32 reads row
+// 32*iw + l of word jw, lane l >= 32 the same row of word jw + 1 (2:4 codes
+// are first expanded to keep bits); one ballot per bit position then yields,
+// for every column, its 32 keep bits.
 template <bool TWO_FOUR>
 __global__ __launch_bounds__(NT) void transpose_kernel(const uint32_t* __restrict__ in, int64_t R, int C, int wpr,
                                                        int wprT, uint32_t* __restrict__ out) {
