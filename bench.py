@@ -123,9 +123,12 @@ def traffic_summary(workload: str, fetch_csv: str, write_csv: str, commands=()) 
     def per_kernel(path, counter):
         rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
         rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        # the calibration copy is the probe's large one (mask preparation may
+        # add small copies of its own, e.g. the 2:4 validity flag)
         copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
-        if len(copy) != 1:
-            raise ValueError(f"{path}: expected one calibration copy, found {len(copy)}")
+        copy = [max(copy)] if copy else []
+        if not copy or copy[0] * 1024 < COPY_BYTES / 4:
+            raise ValueError(f"{path}: no calibration copy of {COPY_BYTES} bytes found")
         vals = {}
         for k in KERNEL_SOURCES:
             v = [float(r["Counter_Value"]) for r in rows if f"::{k}<" in r["Kernel_Name"]]
