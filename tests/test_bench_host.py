@@ -81,3 +81,34 @@ def test_executed_flops_count_the_re_merges():
     # 16 token tiles each re-merge W' in the forward and in dX: 15 extra 2rRC per kernel
     assert ex - alg == 2 * 15 * 2 * r * R * C
     assert costs.executed_flops(R, C, 256, r, 256, 256) == costs.algorithmic_flops(R, C, 256, r)
+
+
+def _pmc_csv(path, counter, rows):
+    """A rocprofv3 counter CSV with the columns traffic_summary reads."""
+    lines = ["Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value"]
+    lines += [f'{i},"{name}",{counter},{value}' for i, (name, value) in enumerate(rows)]
+    path.write_text("\n".join(lines) + "\n")
+
+
+def test_traffic_calibrates_on_the_large_copy(tree):
+    # a 2:4 mask preparation reads back a small flag with a copy of its own
+    # before the probe's calibration copy; the calibration is the large one
+    kib = bench.COPY_BYTES / 1024
+    fwd = "void lors::(anonymous namespace)::fwd_kernel<1, true>(...)"
+    for counter, cal, val in (("FETCH_SIZE", kib / 2, 1000.0), ("WRITE_SIZE", kib, 300.0)):
+        _pmc_csv(tree / f"{counter}.csv", counter,
+                 [("__amd_rocclr_copyBuffer", 0.5), (fwd, 7.0), (fwd, val), (fwd, val),
+                  ("__amd_rocclr_copyBuffer", cal)])
+    text = bench.traffic_summary("w", str(tree / "FETCH_SIZE.csv"), str(tree / "WRITE_SIZE.csv"))
+    line = [l for l in text.splitlines() if l.startswith("fwd_kernel ")][0].split()
+    # fetch scaled by 2 (the copy reads COPY_BYTES as half), write by 1; the
+    # set-up dispatch (7.0) is not one of the last two
+    assert int(line[3]) == round(1000.0 * 1024 * 2 + 300.0 * 1024)
+
+
+def test_traffic_needs_a_calibration_copy(tree):
+    fwd = "void lors::(anonymous namespace)::fwd_kernel<1, true>(...)"
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        _pmc_csv(tree / f"{counter}.csv", counter, [("__amd_rocclr_copyBuffer", 0.5), (fwd, 1.0), (fwd, 1.0)])
+    with pytest.raises(ValueError, match="calibration copy"):
+        bench.traffic_summary("w", str(tree / "FETCH_SIZE.csv"), str(tree / "WRITE_SIZE.csv"))
